@@ -1,0 +1,141 @@
+"""Pins for the schedule enumeration and the DAG model (CPU only).
+
+The paper prints closed-form critical paths for each schedule (Section 3); the
+list-scheduling simulation of the DAG must reproduce them exactly, which pins
+both the visiting orders and the accumulation orders.  Lemma 1's condition is
+checked in both directions, and the fp32 worked example of the Introduction
+pins the ordered fp32 summation that defines the deterministic reduction.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import ordered_sum_f32
+from oracle.schedule import (DESCENDING, NAIVE, SHIFT, SYMSHIFT, Deadlock, Schedule, build,
+                             check, simulate)
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def closed(name, m, n, c, r):
+    expr = golden("makespan_closed_forms.json")["formulas"][name]["expr"]
+    return eval(expr, {"__builtins__": {}}, dict(m=m, n=n, c=c, r=r))
+
+
+def sim(kind, n, m, c, r, causal):
+    s = build(kind, n, n, causal, 64, 64)
+    return simulate([s] * m, n, c, r)
+
+
+@pytest.mark.parametrize("n", [2, 4, 6, 8, 16])
+@pytest.mark.parametrize("m", [2, 4, 6])
+@pytest.mark.parametrize("c,r", [(3, 1), (5, 2), (1, 1), (2, 3)])
+def test_makespans_equal_paper_closed_forms(n, m, c, r):
+    assert sim(NAIVE, n, m, c, r, False) == closed("naive_full", m, n, c, r)
+    assert sim(NAIVE, n, m, c, r, True) == closed("naive_causal", m, n, c, r)
+    # Section 3.3 writes the Descending makespan with "approximately"; the DAG
+    # model meets it exactly while a reduction is no longer than a compute
+    # phase (r <= c), and never beats it otherwise.
+    if r <= c:
+        assert sim(DESCENDING, n, m, c, r, True) == closed("descending_causal", m, n, c, r)
+    else:
+        assert sim(DESCENDING, n, m, c, r, True) >= closed("descending_causal", m, n, c, r)
+    assert sim(SHIFT, n, m, c, r, False) == closed("shift_full", m, n, c, r)
+    assert sim(SYMSHIFT, n, m, c, r, True) == closed("symshift_causal", m, n, c, r)
+
+
+def test_single_head_cases():
+    """m = 1 (outside the even-m formulas): Descending finishes one causal head in
+    n(c+r), Symmetric Shift in (n+1)(c+r) on n SMs; the Fig. 2 toy (n = 2, naive,
+    full mask) loses one reduction to the cross-SM wait."""
+    for n in (4, 8):
+        assert sim(DESCENDING, n, 1, 3, 1, True) == n * 4
+        assert sim(SYMSHIFT, n, 1, 3, 1, True) == (n + 1) * 4
+    c, r = 3, 1
+    assert sim(NAIVE, 2, 1, c, r, False) == 2 * (c + r) + r
+    assert sim(SHIFT, 2, 1, c, r, False) == 2 * (c + r)
+
+
+@pytest.mark.parametrize("t", [2, 4, 6, 8, 16, 32])
+def test_structure(t):
+    """Coverage and KV contiguity for all; conflict-free, depth-monotone
+    accumulation (Lemma 1) for Shift and Symmetric Shift only."""
+    for kind, causal in ((NAIVE, False), (NAIVE, True), (DESCENDING, False), (DESCENDING, True),
+                         (SHIFT, False), (SYMSHIFT, True)):
+        s = build(kind, t, t, causal, 64, 64)
+        props = check(s, t, t, causal, 64, 64)
+        assert props["coverage"] and props["contiguous"], (kind, causal)
+        if kind in (SHIFT, SYMSHIFT):
+            assert props["conflict_free"] and props["monotone"], kind
+        else:
+            assert not props["monotone"], (kind, causal)
+    # Symmetric Shift balances the causal triangle: every chain has t+1 tasks
+    s = build(SYMSHIFT, t, t, True, 64, 64)
+    assert [len(ch) for ch in s.chains] == [t + 1] * (t // 2)
+
+
+@pytest.mark.parametrize("g", [2, 4])
+@pytest.mark.parametrize("tc", [2, 4, 8])
+def test_shift_with_unequal_tiles(g, tc):
+    """T_r = g*T_c Q tiles (smaller Q tiles): the g-tile shift stays
+    conflict-free and depth-monotone; causal naive/descending cover exactly the
+    interacting pairs."""
+    s = build(SHIFT, g * tc, tc, False, 64, 64 * g)
+    props = check(s, g * tc, tc, False, 64, 64 * g)
+    assert all(props.values()), props
+    for kind in (NAIVE, DESCENDING):
+        s = build(kind, g * tc, tc, True, 64, 64 * g)
+        assert check(s, g * tc, tc, True, 64, 64 * g)["coverage"]
+        assert all(len(ch) == g * (tc - j) for j, ch in enumerate(s.chains))
+
+
+def test_lemma1_depth_decreasing_edge_lengthens_critical_path():
+    """Fig. 5 / Lemma 1: swapping two consecutive contributors of one dQ tile in
+    the Shift order creates an edge from a deeper reduction to a shallower one;
+    the checker flags it and the critical path strictly grows."""
+    n, m, c, r = 6, 2, 3, 1
+    base = build(SHIFT, n, n, False, 64, 64)
+    t0 = simulate([base] * m, n, c, r)
+    order = {i: list(js) for i, js in base.order.items()}
+    order[3][1], order[3][2] = order[3][2], order[3][1]
+    bad = Schedule(base.chains, order)
+    assert not check(bad, n, n, False, 64, 64)["monotone"]
+    assert simulate([bad] * m, n, c, r) > t0
+
+
+def test_lemma1_depth_preserving_edges_keep_critical_path():
+    """Sufficiency direction: Shift's ordering edges all satisfy the depth
+    condition, and its makespan equals that of the unconstrained chains
+    (no ordering edges at all), i.e. the edges cost nothing."""
+    n, m, c, r = 8, 4, 3, 1
+    s = build(SHIFT, n, n, False, 64, 64)
+    # With every dQ tile given its own single-contributor "order" there are no
+    # ordering edges left: the makespan is that of the bare chains.
+    bare_chains = [[((i, j), (i, j)) for (j, i) in ch] for ch in s.chains]
+    bare = Schedule(bare_chains, {(i, j): [(i, j)] for i, js in s.order.items() for j in js})
+    assert simulate([bare] * m, n, c, r) == simulate([s] * m, n, c, r) == m * n * (c + r)
+
+
+def test_cyclic_order_is_reported_as_deadlock():
+    """An accumulation order that contradicts the chains' own order (rank 0
+    placed on a task that waits on its successor) can never finish."""
+    s = build(NAIVE, 2, 2, False, 64, 64)
+    # one SM runs chain 0 (KV0: Q0, Q1) to completion before chain 1 (KV1) can
+    # start, but Q0's order puts KV1 first: KV0 waits forever.
+    order = {0: [1, 0], 1: [0, 1]}
+    with pytest.raises(Deadlock):
+        simulate([Schedule(s.chains, order)], 1, 1, 1)
+
+
+def test_fp32_ordered_sum_worked_example():
+    """Introduction: in fp32, (1e8 + 1e-6) - 1e8 = 0 but 1e8 - 1e8 + 1e-6 = 1e-6."""
+    for case in golden("fp32_nonassociativity.json")["cases"]:
+        got = ordered_sum_f32([np.float32(x) for x in case["terms"]])
+        assert got == np.float32(case["fp32_left_to_right"])
