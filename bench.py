@@ -1,0 +1,166 @@
+"""Benchmark: deterministic attention backward on one MI355X.
+
+One step = one full backward call (D = rowsum(dO o O) preprocessing + the main
+kernel with the ordered dQ reduction) over the whole batch of the workload
+B=2, H=16, N=8192, d=128, full mask (16384 tokens, hidden 2048), inputs bf16
+~N(0,1), already resident in HBM.  Reports, as one JSON line:
+
+  value        backward TFLOPS of the deterministic Shift schedule
+               (FLOPs = 4*B*H*N^2*d*2.5, the five-GEMM count)
+  pct_of_atomic that throughput as a percentage of the atomic-add variant's
+  roofline     the main kernel's algorithmic MFMA FLOPs per launch divided by
+               its mean duration (HIP events recorded by the library on the
+               launch stream around that kernel), against the bf16 dense peak
+  cpu_baseline the fp64 oracle timed on the host on one full head of the
+               same workload, scaled to the same FLOP count
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+
+
+class HipEvents:
+    """hipEvent_t pairs via the HIP runtime (for events on the library stream)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        e = ctypes.c_void_p()
+        assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+        return e
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def destroy(self, e):
+        self.hip.hipEventDestroy(e)
+
+
+def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
+    import torch
+    q, k, v, o, do, lse, dq, dk, dv, ws = tensors
+    for _ in range(warmup):
+        dash.dash_attn_bwd(q, k, v, o, do, lse, dq, dk, dv, causal, sched, workspace=ws)
+    pairs = [(ev.create(), ev.create()) for _ in range(steps)]
+    opts = [dash.dash_bwd_options_t(0, 0, None, None, None, a.value, b.value) for a, b in pairs]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        dash.dash_attn_bwd(q, k, v, o, do, lse, dq, dk, dv, causal, sched, workspace=ws, options=opts[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if dash.dash_bwd_check(ws) != dash.DASH_OK:
+        raise RuntimeError(f"{sched}: ordering wait timed out")
+    main_ms = [ev.elapsed_ms(a, b) for a, b in pairs]
+    for a, b in pairs:
+        ev.destroy(a)
+        ev.destroy(b)
+    return wall * 1e3 / steps, sum(main_ms) / len(main_ms)
+
+
+def cpu_baseline(q, k, v, do, causal, flops_per_head):
+    """The oracle, as it is, on one full head (b=0, h=0) of the workload."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    t0 = time.perf_counter()
+    oracle.attn_bwd(q[0, 0], k[0, 0], v[0, 0], do[0, 0], causal)
+    dt = time.perf_counter() - t0
+    return {"value": flops_per_head / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
+            "sample": f"one full head (b=0,h=0) of the workload, fp64 forward recompute + dQ/dK/dV, "
+                      f"{dt:.1f} s; FLOPs counted as 4*N^2*d*2.5 for that head"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--schedule", default="shift")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--N", type=int, default=8192)
+    ap.add_argument("--causal", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the backward shards over heads with no communication, "
+              "and this build runs on a single MI355X; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2601_21824_amd import binding as dash
+    from paper_2601_21824_amd.synth import make_inputs
+
+    dash.load()
+    N, d, causal = args.N, 128, args.causal
+    B = max(1, 16384 // N)
+    H = 32 if causal else 16
+    flops = 4.0 * B * H * N * N * d * 2.5 / (2 if causal else 1)
+    q, k, v, do = make_inputs(B, H, N, d, seed=1234)
+    qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
+    og, lseg = dash.attn_fwd(qg, kg, vg, causal)
+    dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
+    ws = dash.new_workspace(B, H, N, d)
+    torch.cuda.synchronize()
+    tensors = (qg, kg, vg, og, dog, lseg, dq, dk, dv, ws)
+    ev = HipEvents()
+
+    results = {}
+    det = args.schedule
+    for sched in dict.fromkeys([det, "atomic", "naive"]):
+        ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
+        results[sched] = (ms, main_ms, flops / (ms * 1e-3) / 1e12)
+        print(f"[bench] {sched}: {ms:.3f} ms/step, main kernel {main_ms:.3f} ms, "
+              f"{results[sched][2]:.1f} TFLOPS", file=sys.stderr, flush=True)
+
+    ms, main_ms, tflops = results[det]
+    main_tflops = flops / (main_ms * 1e-3) / 1e12
+    out = {
+        "metric": "deterministic attn-bwd TFLOPS (bf16, d=128, N=8192) + % of atomic variant",
+        "value": round(tflops, 2),
+        "unit": "TFLOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"attention backward B={B} H={H} N={N} d={d} "
+                               f"{'causal' if causal else 'full'} mask, {det} schedule",
+                   "B": B, "H": H, "N": N, "d": d, "mask": "causal" if causal else "full",
+                   "schedule": det, "global_batch": B, "seq_len": N},
+        "pct_of_atomic": round(100.0 * tflops / results["atomic"][2], 2),
+        "atomic_tflops": round(results["atomic"][2], 2),
+        "naive_tflops": round(results["naive"][2], 2),
+        "roofline": {"bound": "mfma", "kernel": "bwd_main_kernel<128>",
+                     "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "main_kernel_ms": round(main_ms, 4)},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(q, k, v, do, causal, flops / (B * H))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

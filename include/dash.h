@@ -1,0 +1,171 @@
+/*
+ * dash.h -- C ABI of libdash: deterministic FlashAttention backward for
+ * AMD Instinct MI355X (gfx950), with the dQ reduction order scheduled as in
+ * "DASH: Deterministic Attention Scheduling for High-throughput Reproducible
+ * LLM Training" (arXiv 2601.21824).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *    keeps no pointer after a call returns.
+ *  - q, k, v, o, dO, dq, dk, dv: bf16 values (stored as uint16_t), layout
+ *    [B][H][N][d], row-major and contiguous (one head = an N x d matrix).
+ *  - lse: fp32 [B][H][N], the natural-log logsumexp of the scaled scores of
+ *    each query row (the "logsumexp vector L" that Algorithm 1 takes as input).
+ *  - Self-attention only: N queries attend to N keys.  With causal != 0,
+ *    query i sees key j iff j <= i.
+ *  - d must be 64 or 128.  N >= 0 is arbitrary (ragged last tiles are masked);
+ *    B, H >= 0.  A problem with B*H*N == 0 is a successful no-op.
+ *  - scale is the softmax scale s in S = s * Q K^T (the _ex forms take it;
+ *    the others use 1/sqrt(d)).  dQ and dK include the factor s, dV does not.
+ *  - Calls are asynchronous on the given HIP stream (hipStream_t passed as
+ *    void*; NULL = the default stream) unless stated otherwise.
+ *  - No C++ exception crosses this interface.  Every int-returning function
+ *    returns a dash_status_t; on a non-OK return dash_last_error() gives a
+ *    message (thread-local, valid until the next call from that thread).
+ */
+#ifndef DASH_H
+#define DASH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Order in which the dQ partials of the KV tiles are summed (the schedule). */
+typedef enum {
+  /* fp32 hardware atomic adds, order = completion order: NOT deterministic.
+     The conventional backward the paper starts from (Background section). */
+  DASH_SCHED_ATOMIC = 0,
+  /* every KV tile visits its Q tiles in ascending order; each dQ tile is summed
+     in ascending KV order (the deterministic baseline, Section 3.2). */
+  DASH_SCHED_NAIVE = 1,
+  /* Descending Q-Tile Iteration (Section 3.3): Q tiles visited last to first,
+     same ascending-KV summation order as NAIVE (so dQ is bitwise equal). */
+  DASH_SCHED_DESCENDING = 2,
+  /* Shift Scheduling (Section 3.4): the workgroup of KV tile j starts at a
+     cyclically shifted Q tile; dQ summed in visiting order.  Full mask.  With
+     a causal mask it selects Symmetric Shift. */
+  DASH_SCHED_SHIFT = 3,
+  /* Symmetric Shift (Section 3.4, causal masks): KV tiles j and T-1-j share a
+     workgroup; two-phase fold.  Causal mask only. */
+  DASH_SCHED_SYMSHIFT = 4,
+  /* SHIFT for full masks; DESCENDING for causal masks at d >= 128, SYMSHIFT
+     below (the paper's recommendation, Section 4.3). */
+  DASH_SCHED_AUTO = 5
+} dash_schedule_t;
+
+typedef enum {
+  DASH_OK = 0,
+  DASH_ERR_INVALID_ARG = -1, /* null pointer, negative size, d not 64/128, bad enum */
+  DASH_ERR_UNSUPPORTED = -2, /* valid request this build cannot run (e.g. SYMSHIFT
+                                with a full mask, too many KV tiles per head) */
+  DASH_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
+  DASH_ERR_TIMEOUT = -4,     /* an ordering wait exceeded its spin limit; outputs
+                                of that call are undefined */
+  DASH_ERR_NO_DEVICE = -5    /* no usable GPU */
+} dash_status_t;
+
+/* Debug / failure-injection flags of dash_bwd_options_t.flags */
+#define DASH_FLAG_POISON_COUNTERS 1 /* start every ordering counter at a value no
+                                       rank ever waits for: each wait times out
+                                       (exercises the watchdog; kernels still exit) */
+
+/* Optional knobs of dash_attn_bwd_ex.  Pass NULL for defaults. */
+typedef struct {
+  /* Polls an ordering wait makes before it gives up and flags a timeout
+     (0 = default, about 2^24 polls).  The kernel always exits. */
+  int spin_limit;
+  /* DASH_FLAG_* bits */
+  int flags;
+  /* If non-NULL: int32 [B*H][ceil(N/64)][T_c], T_c = ceil(N/d) KV tiles.  The
+     workgroup that adds its partial to 64-row dQ block p with order position r
+     writes its KV-tile index at [bh][p][r] (ordering witness). */
+  int32_t* witness;
+  /* If non-NULL: fp32 [B*H][T_c][N][d].  Each KV tile's unscaled dQ partial
+     (its dS K for every query row) is written at [bh][j]. */
+  float* partials;
+  /* If non-NULL: fp32 [B*H][N][d].  Receives the final unscaled fp32 dQ sum
+     (deterministic schedules only). */
+  float* dq_accum;
+  /* If both non-NULL: hipEvent_t handles (passed as void*) recorded on the
+     call's stream immediately before and after the main backward kernel, so
+     a caller can time that kernel alone. */
+  void* event_main_begin;
+  void* event_main_end;
+} dash_bwd_options_t;
+
+/*
+ * Forward attention producing O and L (Algorithm 1's inputs): O = softmax(s QK^T
+ * + mask) V in bf16, lse = logsumexp per query row in fp32.  Deterministic.
+ * Synchronous with respect to the host on the default stream is NOT implied:
+ * the plain form runs on the default stream asynchronously.
+ */
+int dash_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                  int B, int H, int N, int d, int causal);
+int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse,
+                     int B, int H, int N, int d, int causal, float scale, void* stream);
+
+/*
+ * Attention backward (Algorithm 1): from Q, K, V, O, dO and L computes
+ * D = rowsum(dO o O), then dQ, dK, dV.  Each KV tile's workgroup keeps dK_j,
+ * dV_j on chip; the dQ partials are summed into an fp32 buffer in the order
+ * fixed by `schedule`, serialized by per-Q-block counters (no atomics on the
+ * data), except for DASH_SCHED_ATOMIC.
+ *
+ * The plain form uses a library-owned workspace (grown on demand, freed by
+ * dash_release_workspace), runs on the default stream and SYNCHRONIZES before
+ * returning so that it can report DASH_ERR_TIMEOUT.
+ */
+int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dO,
+                  const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,
+                  int causal, int schedule);
+
+/* Bytes of device workspace dash_attn_bwd_ex needs for this problem (0 if the
+   arguments are invalid).  Independent of the schedule. */
+size_t dash_bwd_workspace_size(int B, int H, int N, int d);
+
+/*
+ * Asynchronous backward on `stream` with a caller-provided device workspace of
+ * ws_bytes >= dash_bwd_workspace_size(B,H,N,d) bytes (256-byte aligned).  The
+ * workspace must not be used by another call until this one has finished.
+ * A wait timeout is recorded in the workspace; read it with dash_bwd_check.
+ */
+int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO,
+                     const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,
+                     int causal, int schedule, float scale, void* workspace, size_t ws_bytes,
+                     const dash_bwd_options_t* opts, void* stream);
+
+/* Synchronizes `stream`, then returns DASH_ERR_TIMEOUT if the last backward
+   that used `workspace` hit a wait timeout, DASH_OK otherwise. */
+int dash_bwd_check(void* workspace, void* stream);
+
+/* The concrete schedule DASH_SCHED_AUTO / SHIFT resolve to for (d, causal). */
+int dash_resolve_schedule(int schedule, int d, int causal);
+
+/*
+ * Host-side view of the schedule the kernels follow (no GPU needed).  For one
+ * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c
+ * KV tiles of bc = d rows.  Writes, when the pointer is non-NULL:
+ *   geometry[4]            = {T_r, T_c, br, number of workgroups per head}
+ *   chain_len[w]           = tasks of workgroup w
+ *   task_kv[w*cap + t], task_q[w*cap + t] = the t-th task of workgroup w,
+ *                            cap = max chain length = geometry-dependent
+ *                            (use T_r + 1)
+ *   rank[i*T_c + j]        = position of KV tile j in Q tile i's summation
+ *                            order (-1 when they do not interact)
+ * Returns a dash_status_t.
+ */
+int dash_schedule_table(int schedule, int N, int d, int causal, int* geometry, int* chain_len,
+                        int* task_kv, int* task_q, int* rank);
+
+const char* dash_last_error(void);
+/* Frees the library-owned workspace of dash_attn_bwd (next call reallocates). */
+void dash_release_workspace(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DASH_H */

@@ -1,0 +1,295 @@
+// dash_api.hip -- the C ABI declared in include/dash.h: argument checking,
+// schedule resolution, workspace layout, kernel launches and error reporting.
+// Host code only; the kernels live in attn_fwd.hip and attn_bwd.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "dash.h"
+#include "kernels.h"
+#include "schedule.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(DASH_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t ctrl, dqacc, dvec, counters, total;
+};
+
+// ctrl first so that dash_bwd_check can find it without the problem size
+Layout layout(int B, int H, int N, int d) {
+  Layout L;
+  const size_t bh = (size_t)B * H;
+  const size_t nblk = ((size_t)N + dash::kBlockRows - 1) / dash::kBlockRows;
+  size_t off = 0;
+  L.ctrl = off;
+  off += dash::kCtrlBytes;
+  L.dqacc = off;
+  off += align256(bh * N * d * sizeof(float));
+  L.dvec = off;
+  off += align256(bh * N * sizeof(float));
+  L.counters = off;
+  off += align256(bh * nblk * dash::kCtrStride * sizeof(int));
+  L.total = off;
+  return L;
+}
+
+struct DeviceInfo {
+  int device = -1;
+  int cus = 0;
+  int occ64 = 0, occ128 = 0;
+};
+
+std::mutex g_mu;
+DeviceInfo g_dev[64];
+
+int device_info(DeviceInfo* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DASH_ERR_NO_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(DASH_ERR_NO_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lk(g_mu);
+  DeviceInfo& di = g_dev[dev];
+  if (di.device < 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+      return fail(DASH_ERR_NO_DEVICE, std::string("libdash is built for gfx950, device is ") + prop.gcnArchName);
+    di.cus = prop.multiProcessorCount;
+    di.occ64 = dash::bwd_main_occupancy(64);
+    di.occ128 = dash::bwd_main_occupancy(128);
+    if (di.occ64 <= 0 || di.occ128 <= 0) return fail(DASH_ERR_HIP, "occupancy query failed");
+    di.device = dev;
+  }
+  *out = di;
+  return DASH_OK;
+}
+
+int check_shape(int B, int H, int N, int d) {
+  if (B < 0 || H < 0 || N < 0) return fail(DASH_ERR_INVALID_ARG, "B, H and N must be >= 0");
+  if (d != 64 && d != 128) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  if ((double)N * d * 4 >= 2147483648.0) return fail(DASH_ERR_INVALID_ARG, "N*d too large (per-head fp32 > 2 GiB)");
+  if ((double)B * H >= 2147483647.0 / 1024) return fail(DASH_ERR_INVALID_ARG, "B*H too large");
+  return DASH_OK;
+}
+
+int resolve(int schedule, int d, int causal) {
+  switch (schedule) {
+    case DASH_SCHED_AUTO:
+      return !causal ? DASH_SCHED_SHIFT : (d >= 128 ? DASH_SCHED_DESCENDING : DASH_SCHED_SYMSHIFT);
+    case DASH_SCHED_SHIFT:
+      return causal ? DASH_SCHED_SYMSHIFT : DASH_SCHED_SHIFT;
+    default:
+      return schedule;
+  }
+}
+
+int check_schedule(int schedule, int causal) {
+  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_AUTO)
+    return fail(DASH_ERR_INVALID_ARG, "unknown schedule");
+  if (schedule == DASH_SCHED_SYMSHIFT && !causal)
+    return fail(DASH_ERR_UNSUPPORTED, "symmetric shift is the causal-mask schedule; use SHIFT for a full mask");
+  return DASH_OK;
+}
+
+// everything about a backward call that can be checked without the device
+int check_bwd(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
+              const void* dq, const void* dk, const void* dv, int B, int H, int N, int d, int causal,
+              int schedule, float scale) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if ((rc = check_schedule(schedule, causal))) return rc;
+  if ((size_t)B * H * N == 0) return DASH_OK;
+  if (!q || !k || !v || !o || !dO || !lse || !dq || !dk || !dv)
+    return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(DASH_ERR_INVALID_ARG, "scale must be finite and > 0");
+  return DASH_OK;
+}
+
+void* g_ws = nullptr;
+size_t g_ws_bytes = 0;
+std::mutex g_ws_mu;
+
+}  // namespace
+
+extern "C" {
+
+const char* dash_last_error(void) { return g_err.c_str(); }
+
+int dash_resolve_schedule(int schedule, int d, int causal) { return resolve(schedule, d, causal); }
+
+size_t dash_bwd_workspace_size(int B, int H, int N, int d) {
+  if (check_shape(B, H, N, d) != DASH_OK) return 0;
+  return layout(B, H, N, d).total;
+}
+
+int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N,
+                     int d, int causal, float scale, void* stream) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if ((size_t)B * H * N == 0) return DASH_OK;
+  if (!q || !k || !v || !o || !lse) return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(DASH_ERR_INVALID_ARG, "scale must be finite and > 0");
+  DeviceInfo di;
+  if ((rc = device_info(&di))) return rc;
+  dash::FwdArgs a{q, k, v, o, lse, B * H, N, causal ? 1 : 0, scale};
+  hipError_t e = dash::launch_attn_fwd(a, d, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
+  return DASH_OK;
+}
+
+int dash_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N, int d,
+                  int causal) {
+  if (d <= 0) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  return dash_attn_fwd_ex(q, k, v, o, lse, B, H, N, d, causal, 1.0f / std::sqrt((float)d), nullptr);
+}
+
+int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
+                     void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule,
+                     float scale, void* workspace, size_t ws_bytes, const dash_bwd_options_t* opts,
+                     void* stream) {
+  int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
+  if (rc) return rc;
+  if ((size_t)B * H * N == 0) return DASH_OK;
+  const Layout L = layout(B, H, N, d);
+  if (!workspace || ws_bytes < L.total)
+    return fail(DASH_ERR_INVALID_ARG, "workspace missing or smaller than dash_bwd_workspace_size()");
+  if (((uintptr_t)workspace & 255) != 0) return fail(DASH_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (opts && opts->spin_limit < 0) return fail(DASH_ERR_INVALID_ARG, "spin_limit must be >= 0");
+  DeviceInfo di;
+  if ((rc = device_info(&di))) return rc;
+
+  const int sched = resolve(schedule, d, causal);
+  const dash::Geom G = dash::make_geom(sched, causal, N, d);
+  const int occ = d == 64 ? di.occ64 : di.occ128;
+  const long resident = (long)occ * di.cus;
+  // Every chain of one head must be able to run at once: a chain may wait on
+  // any other chain of its head (persistent grid, in-order work tickets).
+  if (sched != DASH_SCHED_ATOMIC && G.chains > resident)
+    return fail(DASH_ERR_UNSUPPORTED, "too many KV tiles per head for the resident workgroups of this GPU");
+  const long items = (long)B * H * G.chains;
+  const int grid = (int)(items < resident ? items : resident);
+
+  char* ws = (char*)workspace;
+  dash::BwdArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.dO = dO;
+  a.lse = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.dqacc = (float*)(ws + L.dqacc);
+  a.dvec = (float*)(ws + L.dvec);
+  a.counters = (int*)(ws + L.counters);
+  a.ctrl = (int*)(ws + L.ctrl);
+  a.witness = opts ? opts->witness : nullptr;
+  a.partials = opts ? opts->partials : nullptr;
+  a.dq_accum = opts ? opts->dq_accum : nullptr;
+  a.bh = B * H;
+  a.n = N;
+  a.nblk = (N + dash::kBlockRows - 1) / dash::kBlockRows;
+  a.tc = (N + d - 1) / d;
+  a.scale = scale;
+  a.spin_limit = (opts && opts->spin_limit > 0) ? opts->spin_limit : (1 << 24);
+  a.poison = (opts && (opts->flags & DASH_FLAG_POISON_COUNTERS)) ? 1 : 0;
+  a.G = G;
+  const bool timed = opts && opts->event_main_begin && opts->event_main_end;
+  a.ev_begin = timed ? (hipEvent_t)opts->event_main_begin : nullptr;
+  a.ev_end = timed ? (hipEvent_t)opts->event_main_end : nullptr;
+  hipError_t e = dash::launch_bwd(a, d, grid, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "backward launch");
+  return DASH_OK;
+}
+
+int dash_bwd_check(void* workspace, void* stream) {
+  if (!workspace) return fail(DASH_ERR_INVALID_ARG, "null workspace");
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int flag = 0;
+  e = hipMemcpy(&flag, (char*)workspace + dash::kCtrlError * sizeof(int), sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "reading the error flag");
+  if (flag) return fail(DASH_ERR_TIMEOUT, "an ordering wait exceeded its spin limit");
+  return DASH_OK;
+}
+
+int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
+                  void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule) {
+  if (d != 64 && d != 128) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  const float scale = 1.0f / std::sqrt((float)d);
+  int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
+  if (rc) return rc;
+  if ((size_t)B * H * N == 0) return DASH_OK;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  const size_t need = layout(B, H, N, d).total;
+  if (g_ws_bytes < need) {
+    if (g_ws) (void)hipFree(g_ws);
+    g_ws = nullptr;
+    g_ws_bytes = 0;
+    hipError_t e = hipMalloc(&g_ws, need);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+    g_ws_bytes = need;
+  }
+  rc = dash_attn_bwd_ex(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale, g_ws,
+                        g_ws_bytes, nullptr, nullptr);
+  if (rc) return rc;
+  return dash_bwd_check(g_ws, nullptr);
+}
+
+void dash_release_workspace(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  if (g_ws) (void)hipFree(g_ws);
+  g_ws = nullptr;
+  g_ws_bytes = 0;
+}
+
+int dash_schedule_table(int schedule, int N, int d, int causal, int* geometry, int* chain_len, int* task_kv,
+                        int* task_q, int* rank) {
+  int rc = check_shape(1, 1, N, d);
+  if (rc) return rc;
+  if ((rc = check_schedule(schedule, causal))) return rc;
+  const int sched = resolve(schedule, d, causal);
+  const dash::Geom G = dash::make_geom(sched, causal, N, d);
+  if (geometry) {
+    geometry[0] = G.t_r;
+    geometry[1] = G.t_c;
+    geometry[2] = G.br;
+    geometry[3] = G.chains;
+  }
+  const int cap = G.t_r + 1;
+  for (int w = 0; w < G.chains; ++w) {
+    const int len = dash::chain_len(G, w);
+    if (chain_len) chain_len[w] = len;
+    for (int t = 0; t < len; ++t) {
+      int j, i;
+      dash::task(G, w, t, &j, &i);
+      if (task_kv) task_kv[(size_t)w * cap + t] = j;
+      if (task_q) task_q[(size_t)w * cap + t] = i;
+    }
+  }
+  if (rank)
+    for (int i = 0; i < G.t_r; ++i)
+      for (int j = 0; j < G.t_c; ++j)
+        rank[(size_t)i * G.t_c + j] = dash::interacts(G, i, j) ? dash::rank_of(G, i, j) : -1;
+  return DASH_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// kernels.h -- interface between the C ABI layer and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "schedule.h"
+
+namespace dash {
+
+constexpr int kCtrStride = 32;        // ints per ordering counter (one 128-byte line each)
+constexpr int kPoison = 0x40000000;   // counter start value no rank waits for
+constexpr int kCtrlTicket = 0;        // ctrl[] slot: next work item
+constexpr int kCtrlError = 16;        // ctrl[] slot: set to 1 when a wait timed out
+constexpr size_t kCtrlBytes = 256;    // ctrl block at the start of the workspace
+
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  int bh, n, causal;
+  float scale;
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dO;
+  const float* lse;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dqacc;   // [bh][N][d] fp32 accumulator
+  float* dvec;    // [bh][N] D = rowsum(dO o O)
+  int* counters;  // [bh][nblk] ordering counters, kCtrStride ints apart
+  int* ctrl;      // ticket / error flag
+  int32_t* witness;
+  float* partials;
+  float* dq_accum;
+  int bh, n, nblk, tc;  // tc = real KV tiles per head (ceil(N/d))
+  float scale;
+  int spin_limit;
+  int poison;
+  Geom G;
+  hipEvent_t ev_begin, ev_end;  // optional, recorded around bwd_main
+};
+
+hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream);
+hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream);
+int bwd_main_occupancy(int d);
+
+}  // namespace dash

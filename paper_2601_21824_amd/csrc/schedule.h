@@ -1,0 +1,141 @@
+// schedule.h -- closed-form dQ-reduction schedules, usable on host and device.
+//
+// One attention head of N rows is cut into KV tiles of BC = d rows (one
+// workgroup's resident K_j, V_j, dK_j, dV_j) and scheduling Q tiles of br rows;
+// a scheduling Q tile is processed as br/64 physical 64-row blocks, each with
+// its own ordering counter.  A workgroup runs a "chain" of tasks (KV tile j,
+// Q tile i); the dQ partials of Q tile i are added in the order rank(i, j).
+//
+//  NAIVE       -- ascending Q tiles; dQ summed in ascending KV order
+//                 (the deterministic baseline analysed in Section 3.2).
+//  DESCENDING  -- Descending Q-Tile Iteration (Section 3.3): Q tiles from last
+//                 to first, summation order unchanged (ascending KV).
+//  SHIFT       -- Shift Scheduling (Section 3.4, full mask): workgroup j visits
+//                 Q tiles (j*g + t) mod T_r, g = T_r / T_c; the summation order is
+//                 the visiting order, so rank = (i/g - j) mod T_c.
+//  SYMSHIFT    -- Symmetric Shift (Section 3.4, causal): workgroup p owns KV tiles
+//                 p and T-1-p (T even, h = T/2).  Phase 1 (steps 0..h-1): Q tile
+//                 h + (p+t) mod h with KV p (dense lower-left rectangle).  Phase 2
+//                 (steps h..2h): KV p over Q tiles p..h-1 top-down, then KV T-1-p
+//                 over Q tiles T-1 down to T-1-p.  The summation order is the
+//                 visiting order: rank = i-j for i < h; for i >= h,
+//                 (i-h-j) mod h when j < h and j when j >= h.
+//  ATOMIC      -- NAIVE's iteration order, unordered fp32 atomic adds.
+//
+// Padding: with a causal mask every schedule uses br = BC; T_r = g*T_c always
+// (Q tiles past N are empty and skipped); SYMSHIFT rounds T up to even with an
+// empty KV/Q tile, which touches no real dQ tile.
+#pragma once
+
+#if defined(__HIPCC__)
+#define DASH_HD __host__ __device__ inline
+#else
+#define DASH_HD inline
+#endif
+
+namespace dash {
+
+enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4 };
+
+constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
+
+struct Geom {
+  int sched;   // Sched
+  int causal;  // 0/1
+  int bc;      // rows per KV tile (= head dim)
+  int br;      // rows per scheduling Q tile (64, or bc when causal)
+  int g;       // bc / br
+  int t_c;     // KV tiles per head (SYMSHIFT: rounded up to even)
+  int t_r;     // scheduling Q tiles per head (= g * t_c)
+  int nsub;    // physical 64-row blocks per scheduling Q tile (= br / 64)
+  int chains;  // workgroup chains per head
+};
+
+DASH_HD Geom make_geom(int sched, int causal, int N, int d) {
+  Geom G;
+  G.sched = sched;
+  G.causal = causal ? 1 : 0;
+  G.bc = d;
+  G.br = causal ? d : kBlockRows;
+  G.g = G.bc / G.br;
+  G.t_c = (N + G.bc - 1) / G.bc;
+  if (sched == S_SYMSHIFT) G.t_c += G.t_c & 1;
+  G.t_r = G.g * G.t_c;
+  G.nsub = G.br / kBlockRows;
+  G.chains = sched == S_SYMSHIFT ? G.t_c / 2 : G.t_c;
+  return G;
+}
+
+// first Q tile that interacts with KV tile j
+DASH_HD int first_q(const Geom& G, int j) { return G.causal ? (j * G.bc) / G.br : 0; }
+
+DASH_HD bool interacts(const Geom& G, int i, int j) {
+  return !G.causal || (i + 1) * G.br - 1 >= j * G.bc;
+}
+
+// number of KV tiles whose partials are summed into Q tile i
+DASH_HD int contributors(const Geom& G, int i) {
+  if (!G.causal) return G.t_c;
+  int c = ((i + 1) * G.br - 1) / G.bc + 1;
+  return c < G.t_c ? c : G.t_c;
+}
+
+DASH_HD int chain_len(const Geom& G, int w) {
+  if (G.sched == S_SYMSHIFT) return G.t_r + 1;
+  if (G.sched == S_SHIFT) return G.t_r;
+  return G.t_r - first_q(G, w);
+}
+
+DASH_HD int pmod(int a, int m) {
+  int r = a % m;
+  return r < 0 ? r + m : r;
+}
+
+// t-th task of chain w: KV tile *j, Q tile *i
+DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
+  switch (G.sched) {
+    case S_DESCENDING:
+      *j = w;
+      *i = G.t_r - 1 - t;
+      return;
+    case S_SHIFT:
+      *j = w;
+      *i = pmod(w * G.g + t, G.t_r);
+      return;
+    case S_SYMSHIFT: {
+      const int h = G.t_r / 2;
+      if (t < h) {
+        *j = w;
+        *i = h + pmod(w + t, h);
+      } else if (t - h <= h - 1 - w) {
+        *j = w;
+        *i = w + (t - h);
+      } else {
+        *j = G.t_r - 1 - w;
+        *i = 3 * h - 1 - (t - h) - w;
+      }
+      return;
+    }
+    default:  // NAIVE, ATOMIC
+      *j = w;
+      *i = first_q(G, w) + t;
+      return;
+  }
+}
+
+// position of KV tile j in Q tile i's summation order
+DASH_HD int rank_of(const Geom& G, int i, int j) {
+  switch (G.sched) {
+    case S_SHIFT:
+      return pmod(i / G.g - j, G.t_c);
+    case S_SYMSHIFT: {
+      const int h = G.t_r / 2;
+      if (i < h) return i - j;
+      return j < h ? pmod(i - h - j, h) : j;
+    }
+    default:
+      return j;
+  }
+}
+
+}  // namespace dash

@@ -1,0 +1,101 @@
+"""C-ABI checks that need no GPU: the library loads and exports every symbol
+the header declares, argument errors are reported before any device work, and
+the schedule the kernels follow equals the oracle's independent enumeration
+(bit-exact integer tables)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import schedule as osched
+from paper_2601_21824_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "dash.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dash_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = b.load()
+    names = header_functions()
+    assert set(names) == set(b.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def call_bwd(lib, ptr, B=1, H=1, N=128, d=64, causal=0, sched=1):
+    p = [ctypes.c_void_p(ptr)] * 9
+    return lib.dash_attn_bwd(*p, B, H, N, d, causal, sched)
+
+
+def test_argument_errors_without_device():
+    lib = b.load()
+    assert call_bwd(lib, 0) == b.DASH_ERR_INVALID_ARG  # null pointers
+    assert call_bwd(lib, 4096, d=96) == b.DASH_ERR_INVALID_ARG
+    assert call_bwd(lib, 4096, N=-1) == b.DASH_ERR_INVALID_ARG
+    assert call_bwd(lib, 4096, sched=9) == b.DASH_ERR_INVALID_ARG
+    assert call_bwd(lib, 4096, sched=b.DASH_SCHED_SYMSHIFT, causal=0) == b.DASH_ERR_UNSUPPORTED
+    assert "symmetric shift" in b.dash_last_error()
+    # empty problems are successful no-ops, even with null pointers
+    assert call_bwd(lib, 0, N=0) == b.DASH_OK
+    assert call_bwd(lib, 0, B=0) == b.DASH_OK
+    assert lib.dash_attn_fwd(*([ctypes.c_void_p(0)] * 5), 1, 1, 0, 64, 0) == b.DASH_OK
+    assert lib.dash_attn_fwd(*([ctypes.c_void_p(0)] * 5), 1, 1, 8, 64, 0) == b.DASH_ERR_INVALID_ARG
+    assert b.dash_bwd_workspace_size(1, 1, 100, 96) == 0
+    assert b.dash_bwd_workspace_size(2, 16, 8192, 128) >= 2 * 16 * 8192 * 128 * 4
+    assert lib.dash_bwd_check(ctypes.c_void_p(0), ctypes.c_void_p(0)) == b.DASH_ERR_INVALID_ARG
+    # explicit-workspace form: too small a workspace is an argument error
+    opts = b.dash_bwd_options_t(0, 0, None, None, None, None, None)
+    p = [ctypes.c_void_p(4096)] * 9
+    rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
+                              16, ctypes.byref(opts), None)
+    assert rc == b.DASH_ERR_INVALID_ARG
+
+
+def test_schedule_resolution():
+    assert b.dash_resolve_schedule("auto", 128, False) == b.DASH_SCHED_SHIFT
+    assert b.dash_resolve_schedule("auto", 128, True) == b.DASH_SCHED_DESCENDING
+    assert b.dash_resolve_schedule("auto", 64, True) == b.DASH_SCHED_SYMSHIFT
+    assert b.dash_resolve_schedule("shift", 64, True) == b.DASH_SCHED_SYMSHIFT
+    assert b.dash_resolve_schedule("naive", 64, True) == b.DASH_SCHED_NAIVE
+
+
+KINDS = {b.DASH_SCHED_NAIVE: osched.NAIVE, b.DASH_SCHED_DESCENDING: osched.DESCENDING,
+         b.DASH_SCHED_SHIFT: osched.SHIFT, b.DASH_SCHED_SYMSHIFT: osched.SYMSHIFT,
+         b.DASH_SCHED_ATOMIC: osched.NAIVE}
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 8192, 16384])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("sched", [0, 1, 2, 3, 4])
+def test_schedule_table_matches_oracle(sched, causal, N, d):
+    if sched == b.DASH_SCHED_SYMSHIFT and not causal:
+        pytest.skip("symshift is causal-only")
+    tab = b.dash_schedule_table(sched, N, d, causal)
+    concrete = b.dash_resolve_schedule(sched, d, causal)
+    kind = KINDS[concrete]
+    t_r, t_c, br = tab["t_r"], tab["t_c"], tab["br"]
+    # tile sizes: KV tiles of d rows; Q tiles of 64 rows (full) or d rows (causal)
+    assert br == (d if causal else 64) and t_r * br == t_c * d
+    ref = osched.build(kind, t_r, t_c, causal, br, d)
+    assert tab["chains"] == len(ref.chains)
+    for w, ch in enumerate(ref.chains):
+        n = tab["chain_len"][w]
+        assert n == len(ch)
+        got = list(zip(tab["task_kv"][w][:n].tolist(), tab["task_q"][w][:n].tolist()))
+        assert got == ch, (w, got, ch)
+    want = np.full((t_r, t_c), -1)
+    for i, js in ref.order.items():
+        for r, j in enumerate(js):
+            want[i, j] = r
+    np.testing.assert_array_equal(tab["rank"], want)
+    if kind in (osched.SHIFT, osched.SYMSHIFT):
+        props = osched.check(ref, t_r, t_c, causal, br, d)
+        assert props["conflict_free"] and props["monotone"]

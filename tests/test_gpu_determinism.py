@@ -1,0 +1,148 @@
+"""GPU tests of the ordered reduction itself: bitwise run-to-run determinism,
+the ordering witness against the oracle's accumulation order, an exact replay
+of the fp32 summation from the exported partials, NAIVE == DESCENDING on dQ,
+and the wait watchdog (forced from the host)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import schedule as osched
+from gpu_util import inputs, run_bwd, run_fwd
+from paper_2601_21824_amd import binding as dash
+
+pytestmark = pytest.mark.gpu
+
+DET_CASES = [
+    (4, 16, 1024, 64, True, "naive"),
+    (4, 16, 1024, 64, True, "descending"),
+    (4, 16, 1024, 64, True, "symshift"),
+    (1, 1, 256, 64, False, "shift"),
+    (2, 4, 2048, 128, False, "shift"),
+    (2, 4, 2048, 128, False, "naive"),
+    (2, 4, 2048, 128, True, "descending"),
+    (2, 4, 2048, 128, True, "symshift"),
+]
+
+
+@pytest.mark.parametrize("case", DET_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in DET_CASES])
+def test_bitwise_identical_over_100_runs(case):
+    B, H, N, d, causal, sched = case
+    print(f"\n[determinism] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=77)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d)
+    first = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
+    outs = [torch.empty_like(t) for t in first]
+    for r in range(99):
+        dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, *outs, causal, sched, workspace=ws)
+        torch.cuda.synchronize()
+        for a, b in zip(first, outs):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"run {r + 2} differs"
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+
+
+@pytest.mark.parametrize("N,d", [(1024, 64), (2048, 128)])
+def test_naive_and_descending_give_identical_dq(N, d):
+    """Both sum every dQ tile in ascending KV order from identical partials."""
+    B, H = 2, 4
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=9)
+    og, lseg = run_fwd(qg, kg, vg, True)
+    dq1, _, _ = run_bwd(qg, kg, vg, og, dog, lseg, True, "naive")
+    dq2, _, _ = run_bwd(qg, kg, vg, og, dog, lseg, True, "descending")
+    assert torch.equal(dq1.view(torch.int16), dq2.view(torch.int16))
+
+
+PROTO_CASES = [
+    (1, 2, 512, 128, False, "shift"),
+    (1, 2, 512, 128, False, "naive"),
+    (1, 2, 576, 64, True, "symshift"),
+    (1, 2, 512, 128, True, "symshift"),
+    (1, 2, 512, 128, True, "descending"),
+    (2, 1, 300, 64, True, "symshift"),
+    (2, 1, 300, 128, False, "shift"),
+]
+
+
+@pytest.mark.parametrize("case", PROTO_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in PROTO_CASES])
+def test_witness_and_partial_sum_replay(case):
+    """The order the workgroups actually added their partials in equals the
+    oracle's order, and summing the exported partials in that order in fp32
+    reproduces the accumulator bit for bit (and dQ = bf16(scale * acc))."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[protocol] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=21)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    nblk = (N + 63) // 64
+    tc = (N + d - 1) // d
+    witness = torch.full((B * H, nblk, tc), -1, dtype=torch.int32, device="cuda")
+    partials = torch.full((B * H, tc, N, d), float("nan"), dtype=torch.float32, device="cuda")
+    acc = torch.full((B * H, N, d), float("nan"), dtype=torch.float32, device="cuda")
+    opts = dash.dash_bwd_options_t(0, 0, witness.data_ptr(), partials.data_ptr(), acc.data_ptr(), None, None)
+    dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts)
+    tab = dash.dash_schedule_table(sched, N, d, causal)
+    kind = {"shift": osched.SHIFT, "naive": osched.NAIVE, "descending": osched.DESCENDING,
+            "symshift": osched.SYMSHIFT}[sched]
+    ref = osched.build(kind, tab["t_r"], tab["t_c"], causal, tab["br"], d)
+    nsub = tab["br"] // 64
+    W = witness.cpu().numpy()
+    P = partials.cpu().numpy()
+    A = acc.cpu().numpy()
+    scale = np.float32(1.0 / np.sqrt(d))
+    for bh in range(B * H):
+        for pb in range(nblk):
+            order = [j for j in ref.order[pb // nsub] if j < tc]
+            assert W[bh, pb, :len(order)].tolist() == order, (bh, pb)
+            assert (W[bh, pb, len(order):] == -1).all()
+            rows = slice(pb * 64, min(N, pb * 64 + 64))
+            want = oracle.ordered_sum_f32([P[bh, j, rows] for j in order])
+            assert np.array_equal(want.view(np.int32), A[bh, rows].view(np.int32)), (bh, pb)
+    want_dq = torch.from_numpy(A * scale).to(torch.bfloat16)
+    assert torch.equal(want_dq.view(torch.int16), dq.cpu().reshape(B * H, N, d).view(torch.int16))
+
+
+def test_watchdog_reports_timeout_and_library_recovers():
+    """Counters poisoned from the host: every first wait times out after a few
+    polls, the kernels still exit, the call reports DASH_ERR_TIMEOUT, and the
+    next ordinary call is correct."""
+    B, H, N, d, causal = 1, 2, 512, 64, False
+    q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=3)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d)
+    opts = dash.dash_bwd_options_t(64, dash.DASH_FLAG_POISON_COUNTERS, None, None, None, None, None)
+    dq, dk, dv = (torch.empty_like(t) for t in (qg, kg, vg))
+    dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, dq, dk, dv, causal, "shift", workspace=ws, options=opts)
+    assert dash.dash_bwd_check(ws) == dash.DASH_ERR_TIMEOUT
+    dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, dq, dk, dv, causal, "shift", workspace=ws)
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    from gpu_util import assert_close
+    rdq, rdk, rdv, _, _ = oracle.attn_bwd(q, k, v, do, causal)
+    assert_close("dQ", dq, rdq)
+    assert_close("dK", dk, rdk)
+
+
+def test_atomic_variant_run_to_run_deviation_reported():
+    """The atomic variant is only reported (cf. Table 1): print the mean over
+    runs of max |dQ_r - dQ_1|; it must still be within tolerance every run."""
+    B, H, N, d, causal = 2, 16, 2048, 128, True
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=13)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, "atomic")
+    devs = []
+    for _ in range(9):
+        dq, _, _ = run_bwd(qg, kg, vg, og, dog, lseg, causal, "atomic")
+        devs.append(float((dq.float() - ref[0].float()).abs().max()))
+    print(f"\n[atomic] mean max|dQ_r - dQ_1| over 9 runs: {np.mean(devs):.3e}", flush=True)
+
+
+def test_bad_arguments_on_device():
+    B, H, N, d = 1, 1, 128, 64
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=1)
+    og, lseg = run_fwd(qg, kg, vg, False)
+    with pytest.raises(dash.DashError) as e:
+        dash.attn_bwd(qg, kg, vg, og, dog, lseg, False, "symshift")
+    assert e.value.code == dash.DASH_ERR_UNSUPPORTED
+    ws = torch.empty(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(dash.DashError) as e:
+        dash.attn_bwd(qg, kg, vg, og, dog, lseg, False, "shift", workspace=ws)
+    assert e.value.code == dash.DASH_ERR_INVALID_ARG
