@@ -96,43 +96,86 @@ __device__ inline bool wait_turn(const int* ctr, int want, int limit) {
 }
 
 // ---------------------------------------------------------------- bwd_main
+// LDS tiles of bf16 rows are stored in 16-byte chunks with chunk c of row r at
+// c ^ sw16(r): 8 consecutive rows read at the same chunk (MFMA row operands)
+// and 4 consecutive rows read by ds_read_b64_tr_b16 (transposed operands)
+// both hit 32 distinct banks.  The fp32 dQ staging tile uses c ^ (r & 7).
+__device__ inline int sw16(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+template <int D>
+__device__ inline int bf_at(int r, int col) {  // element index in a [rows][D] bf16 tile
+  return r * D + (((col >> 3) ^ sw16(r)) << 3) + (col & 7);
+}
+template <int D>
+__device__ inline int f_at(int r, int col) {  // element index in a [rows][D] fp32 tile (col % 4 == 0)
+  return r * D + (((col >> 2) ^ (r & 7)) << 2);
+}
+
+// 4 bf16 of one column from 4 consecutive rows (gfx950 transpose read): within
+// each group of 16 lanes, lane L addresses row L/4, columns 4*(L%4)..+3 of a
+// 4 x 16 tile and receives column L of it.
+__device__ inline u32x2 tr_read(const __bf16* p) {
+  typedef short s16x4 __attribute__((__vector_size__(8)));
+  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// Direct global -> LDS load of 16 (or 4) bytes per lane: lane i of the wave
+// writes bytes [16i, 16i+16) after the wave-uniform LDS base `dst`.
+typedef __attribute__((address_space(3))) void* lds_ptr;
+__device__ inline void lds_load16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, 0);
+}
+__device__ inline void lds_load16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, kCoherent);
+}
+__device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
+}
+
 template <int D>
 struct MainSmem {
-  static constexpr int BM = kBlockRows;  // 64 query rows per block
-  static constexpr int QP = D + 8;       // padded row of Qs / dOs
-  static constexpr int SP = D + 8;       // padded row of dSs (BC = D columns)
-  __bf16 qs[BM * QP];
-  __bf16 dos[BM * QP];
-  __bf16 qts[D * BM];   // Q^T, chunk-swizzled
-  __bf16 dots[D * BM];  // dO^T, chunk-swizzled
-  __bf16 dss[BM * SP];  // dS (bf16), [q][kv]
-  float ls[BM];         // L * log2(e)
-  float ds[BM];         // D
+  static constexpr int BM = kBlockRows;
+  __bf16 ks[D * D];        // K tile [kv][d] (BC = D rows)
+  __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
+  __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
+  __bf16 dss[BM * D];      // dS (bf16) [q][kv]
+  float acc[BM * D];       // dQ accumulator block [q][d] fp32 (chunk c at c ^ (q & 7))
+  float ls[2][BM];         // L per query row
+  float ds[2][BM];         // D per query row
   int item;
 };
 
 template <int D>
 __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
-  constexpr int NW = D / 32;   // waves
-  constexpr int NT = 64 * NW;  // threads
-  constexpr int BC = D;        // KV rows per tile
+  constexpr int NW = D / 32;    // waves
+  constexpr int NT = 64 * NW;   // threads
+  constexpr int BC = D;         // KV rows per tile
   constexpr int BM = kBlockRows;
-  constexpr int KS = D / 16;   // k-steps over d
-  constexpr int KSC = BC / 16; // k-steps over kv
-  constexpr int NB = D / 32;   // 32-column blocks of d
-  constexpr int QP = MainSmem<D>::QP, SP = MainSmem<D>::SP;
-  constexpr int CPR = D / 8;   // 16-byte chunks per row
-  static_assert(16 * CPR == NT, "one loader unit per thread");
+  constexpr int KS = D / 16;    // k-steps over d
+  constexpr int KSC = BC / 16;  // k-steps over kv
+  constexpr int NB = D / 32;    // 32-column blocks of d
+  constexpr int CPR = D / 8;    // 16-byte bf16 chunks per row
+  constexpr int FCR = D / 4;    // 16-byte fp32 chunks per row
+  constexpr int QLD = BM * CPR / NT;   // direct loads per thread for a Q / dO block
+  constexpr int KLD = BC * CPR / NT;   // ... for the K tile
+  constexpr int ALD = BM * FCR / NT;   // ... for the accumulator block
+  static_assert(NT == 2 * D && QLD == 4 && ALD == 8, "thread/tile shape");
   __shared__ __attribute__((aligned(16))) MainSmem<D> sm;
 
   const Geom G = a.G;
   const int N = a.n;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, g = l >> 5, lc = l & 31;
-  const int lu_c = tid % CPR, lu_rg = tid / CPR;  // loader unit: rows 4rg..4rg+3, cols 8c..8c+7
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 5, lc = l & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int L16 = l & 15, nh = (l >> 4) & 1;  // transpose-read lane roles
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   const int total = a.bh * G.chains;
   const bool ordered = G.sched != S_ATOMIC;
+  // Shift-type orders are conflict-free: the next contributor to a block reaches
+  // it at least one step later, so the counter release can wait until the next
+  // step's barrier, by which time the accumulator stores have drained.
+  const bool deferred = G.sched == S_SHIFT || G.sched == S_SYMSHIFT;
   bool failed = false;  // this wave hit a wait timeout: skip further waits
 
   for (;;) {
@@ -146,40 +189,48 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
     const auto rv = make_rsrc((const __bf16*)a.v + head, hbytes);
     const auto rdo = make_rsrc((const __bf16*)a.dO + head, hbytes);
-    const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
-    const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
-    const auto rdv = make_rsrc((__bf16*)a.dv + head, hbytes);
     const auto racc = make_rsrc(a.dqacc + head, hbytes * 2);
-    const auto rl = make_rsrc(a.lse + (size_t)bh * N, (uint32_t)N * 4);
-    const auto rD = make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
 
     const int nsteps = chain_len(G, wch) * G.nsub;
     int cur_j = -1;
-    bf16x8 kreg[KS], vreg[KS], ktreg[KSC];
+    bf16x8 kreg[KS], vreg[KS];
     f32x16 dkacc[NB], dvacc[NB];
+    int pend_ctr = -1, pend_val = 0;  // deferred counter release
 
-    // prefetch registers for the next Q block
-    u32x4 pq[4], pdo[4];
-    float pl = 0.f, pd = 0.f;
     auto step_block = [&](int st, int* j, int* i, int* pb) {
       task(G, wch, st / G.nsub, j, i);
       *pb = *i * G.nsub + st % G.nsub;
     };
-    auto prefetch = [&](int pb) {
+    auto valid_step = [&](int st) {
+      int j, i, pb;
+      step_block(st, &j, &i, &pb);
+      return pb * BM < N && j * BC < N;
+    };
+    // Q / dO / L / D of block pb into LDS buffer b (asynchronous, vmcnt)
+    auto load_block = [&](int pb, int b) {
       const int q0 = pb * BM;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t off = (uint32_t)((q0 + 4 * lu_rg + r) * D + 8 * lu_c) * 2;
-        pq[r] = ld16(rq, off);
-        pdo[r] = ld16(rdo, off);
+      for (int k = 0; k < QLD; ++k) {
+        const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
+        const uint32_t off = (uint32_t)((q0 + r) * D + 8 * c) * 2;
+        lds_load16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
+        lds_load16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
       }
-      if (tid < BM) {
-        pl = ld4f(rl, (uint32_t)(q0 + tid) * 4);
-        pd = ld4f(rD, (uint32_t)(q0 + tid) * 4);
+      if (w == 0) lds_load4(make_rsrc(a.lse + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(q0 + l) * 4);
+      if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(q0 + l) * 4);
+    };
+    // fp32 accumulator block of rows q0.. into sm.acc (device-coherent loads)
+    auto load_acc = [&](int q0) {
+#pragma unroll
+      for (int k = 0; k < ALD; ++k) {
+        const int slot = k * NT + tid, r = slot / FCR, c = (slot % FCR) ^ (r & 7);
+        lds_load16_coherent(racc, &sm.acc[(k * NT + 64 * w) * 4], (uint32_t)((q0 + r) * D + 4 * c) * 4);
       }
     };
     auto store_dkdv = [&](int j) {
+      const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
+      const auto rdv = make_rsrc((__bf16*)a.dv + head, hbytes);
       const int kv0 = j * BC;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -191,19 +242,20 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           st2(rdk, off, to_bf16(dkacc[nb][r] * a.scale));
         }
     };
-
-    // skip leading empty blocks (Q rows past N, or KV tiles past N)
-    auto valid_step = [&](int st) {
-      int j, i, pb;
-      step_block(st, &j, &i, &pb);
-      return pb * BM < N && j * BC < N;
+    auto release = [&]() {  // all waves' accumulator stores are complete: advance the order
+      if (tid == 0 && pend_ctr >= 0)
+        __hip_atomic_store(ctr_head + (size_t)pend_ctr * kCtrStride, pend_val, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      pend_ctr = -1;
     };
+
     int st = 0;
     while (st < nsteps && !valid_step(st)) ++st;
+    int buf = 0;
     if (st < nsteps) {
       int j0, i0, pb0;
       step_block(st, &j0, &i0, &pb0);
-      prefetch(pb0);
+      load_block(pb0, buf);
     }
 
     for (; st < nsteps;) {
@@ -211,7 +263,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       step_block(st, &j, &i, &pb);
       const int q0 = pb * BM;
 
-      if (j != cur_j) {  // new KV tile: flush the previous one, load operands
+      if (j != cur_j) {  // new KV tile: flush the previous one, load K/V operands
         if (cur_j >= 0) store_dkdv(cur_j);
         cur_j = j;
         const int kv0 = j * BC;
@@ -222,14 +274,12 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           kreg[ks] = as_bf16x8(ld16(rk, off));
           vreg[ks] = as_bf16x8(ld16(rv, off));
         }
+        // K tile into LDS for the transposed (K^T) operand of the dQ product;
+        // the previous tile's readers all passed the last barrier
 #pragma unroll
-        for (int ks = 0; ks < KSC; ++ks) {
-          unsigned short t[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) t[e] = ld2(rk, (uint32_t)((kv0 + 16 * ks + 8 * g + e) * D + 32 * w + lc) * 2);
-          u32x4 pk = {t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16), t[4] | ((unsigned)t[5] << 16),
-                      t[6] | ((unsigned)t[7] << 16)};
-          ktreg[ks] = as_bf16x8(pk);
+        for (int k = 0; k < KLD; ++k) {
+          const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
+          lds_load16(rk, &sm.ks[(k * NT + 64 * w) * 8], (uint32_t)((kv0 + r) * D + 8 * c) * 2);
         }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
@@ -240,36 +290,36 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           }
       }
 
-      // ---- stage the prefetched Q / dO block into LDS
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        *(u32x4*)&sm.qs[(4 * lu_rg + r) * QP + 8 * lu_c] = pq[r];
-        *(u32x4*)&sm.dos[(4 * lu_rg + r) * QP + 8 * lu_c] = pdo[r];
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = 8 * lu_c + e;
-        const int at = d * BM + 4 * (lu_rg ^ tswz(d));
-        u32x2 tq = {pick16(pq[0][e >> 1], pq[1][e >> 1], e & 1), pick16(pq[2][e >> 1], pq[3][e >> 1], e & 1)};
-        u32x2 to = {pick16(pdo[0][e >> 1], pdo[1][e >> 1], e & 1), pick16(pdo[2][e >> 1], pdo[3][e >> 1], e & 1)};
-        *(u32x2*)&sm.qts[at] = tq;
-        *(u32x2*)&sm.dots[at] = to;
-      }
-      if (tid < BM) {
-        sm.ls[tid] = pl * kLog2e;
-        sm.ds[tid] = pd;
-      }
+      // ---- this block's Q / dO (and K) landed in LDS; the other buffer is free
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
 
-      // ---- prefetch the next valid block while this one computes
+      // ---- prefetch the next valid block into the other buffer
       int nst = st + 1;
       while (nst < nsteps && !valid_step(nst)) ++nst;
       if (nst < nsteps) {
         int jn, in_, pbn;
         step_block(nst, &jn, &in_, &pbn);
-        prefetch(pbn);
+        load_block(pbn, buf ^ 1);
       }
 
+      // ---- ordering: poll early; if the turn is already ours, fetch the
+      //      accumulator now so its latency hides behind this block's MFMAs
+      const int rank = rank_of(G, i, j);
+      const bool last = rank == contributors(G, i) - 1;
+      int* ctr = ctr_head + (size_t)pb * kCtrStride;
+      bool have_turn = false;
+      if (ordered && !failed) {
+        const int v0 = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        if (v0 == rank) {
+          have_turn = true;
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+          if (rank > 0) load_acc(q0);
+        }
+      }
+
+      const __bf16* qs = sm.qs[buf];
+      const __bf16* dos = sm.dos[buf];
       // ---- S = Q K^T and dP = dO V^T for this wave's 32 KV columns
       f32x16 s[2], dp[2];
 #pragma unroll
@@ -281,10 +331,9 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 aq = *(const bf16x8*)&sm.qs[(32 * qb + lc) * QP + 16 * ks + 8 * g];
-          const bf16x8 ao = *(const bf16x8*)&sm.dos[(32 * qb + lc) * QP + 16 * ks + 8 * g];
-          s[qb] = mfma32(aq, kreg[ks], s[qb]);
-          dp[qb] = mfma32(ao, vreg[ks], dp[qb]);
+          const int at = bf_at<D>(32 * qb + lc, 16 * ks + 8 * g);
+          s[qb] = mfma32(*(const bf16x8*)&qs[at], kreg[ks], s[qb]);
+          dp[qb] = mfma32(*(const bf16x8*)&dos[at], vreg[ks], dp[qb]);
         }
       }
 
@@ -298,12 +347,12 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
           const int ql = 32 * qb + 8 * rb + 4 * g;
-          const f32x4 L4 = *(const f32x4*)&sm.ls[ql];
-          const f32x4 D4 = *(const f32x4*)&sm.ds[ql];
+          const f32x4 L4 = *(const f32x4*)&sm.ls[buf][ql];
+          const f32x4 D4 = *(const f32x4*)&sm.ds[buf][ql];
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const int r = 4 * rb + c;
-            float p = exp2f(s[qb][r] * c2 - L4[c]);
+            float p = exp2f(__builtin_fmaf(s[qb][r], c2, -L4[c] * kLog2e));
             if (need_mask) {
               const int qg = q0 + ql + c;
               if (kv >= N || (G.causal && kv > qg)) p = 0.f;
@@ -318,18 +367,17 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         dsbf[qb][1] = pack8(dp[qb], 8);
       }
 
-      // ---- dV += P^T dO, dK += dS^T Q  (A operands straight from registers)
+      // ---- dV += P^T dO, dK += dS^T Q: A operands from registers, B operands
+      //      by transposed reads of the row-major Q / dO tiles
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const int d = 32 * nb + lc;
-        const int sw = tswz(d);
+        const int col = 32 * nb + 16 * nh + 4 * (L16 & 3);
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int qb = kk >> 1, half = kk & 1;
-          const int ch = (32 * qb + 16 * half + 4 * g) >> 2;
-          const int a0 = d * BM + 4 * (ch ^ sw), a1 = d * BM + 4 * ((ch + 2) ^ sw);
-          const bf16x8 bo = as_bf16x8(*(const u32x2*)&sm.dots[a0], *(const u32x2*)&sm.dots[a1]);
-          const bf16x8 bq = as_bf16x8(*(const u32x2*)&sm.qts[a0], *(const u32x2*)&sm.qts[a1]);
+          const int row = 32 * qb + 16 * half + 4 * g + (L16 >> 2);
+          const bf16x8 bo = as_bf16x8(tr_read(&dos[bf_at<D>(row, col)]), tr_read(&dos[bf_at<D>(row + 8, col)]));
+          const bf16x8 bq = as_bf16x8(tr_read(&qs[bf_at<D>(row, col)]), tr_read(&qs[bf_at<D>(row + 8, col)]));
           dvacc[nb] = mfma32(pbf[qb][half], bo, dvacc[nb]);
           dkacc[nb] = mfma32(dsbf[qb][half], bq, dkacc[nb]);
         }
@@ -341,87 +389,108 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int ql = 32 * qb + 8 * (r >> 2) + 4 * g + (r & 3);
-          sm.dss[ql * SP + 32 * w + lc] = (__bf16)dp[qb][r];
+          sm.dss[bf_at<D>(ql, 32 * w + lc)] = (__bf16)dp[qb][r];
         }
+      // previous block's accumulator stores (deferred release) and this block's
+      // early accumulator fetch are complete
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
+      release();
 
       // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T
       f32x16 dq[2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) dq[qb][r] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < KSC; ++ks) {
-          const bf16x8 bs = *(const bf16x8*)&sm.dss[(32 * qb + lc) * SP + 16 * ks + 8 * g];
-          dq[qb] = mfma32(ktreg[ks], bs, dq[qb]);
+      for (int ks = 0; ks < KSC; ++ks) {
+        const int krow = 16 * ks + 8 * g + (L16 >> 2);
+        const int kcol = 32 * w + 16 * nh + 4 * (L16 & 3);
+        const bf16x8 ak = as_bf16x8(tr_read(&sm.ks[bf_at<D>(krow, kcol)]), tr_read(&sm.ks[bf_at<D>(krow + 4, kcol)]));
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const bf16x8 bs = *(const bf16x8*)&sm.dss[bf_at<D>(32 * qb + lc, 16 * ks + 8 * g)];
+          dq[qb] = mfma32(ak, bs, dq[qb]);
         }
       }
-      // dq[qb][r] <-> query q0 + 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
+      // dq[qb][r] <-> query 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
 
       if (a.partials) {
         const auto rp = make_rsrc(a.partials + ((size_t)bh * a.tc + j) * N * D, hbytes * 2);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-          for (int rb = 0; rb < 4; ++rb) {
-            const u32x4 v = __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2],
-                                                            dq[qb][4 * rb + 3]});
-            st16(rp, (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g) * 4, v);
-          }
+          for (int rb = 0; rb < 4; ++rb)
+            st16(rp, (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g) * 4,
+                 __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
       }
 
-      if (!ordered) {
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const int q = q0 + 32 * qb + lc;
-          if (q < N) {
-            float* dst = a.dqacc + head + (size_t)q * D + 32 * w + 4 * g;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) atomicAdd(dst + 8 * (r >> 2) + (r & 3), dq[qb][r]);
+      bool add = false;  // accumulate into sm.acc (else: store the partial there)
+      if (ordered) {
+        if (!have_turn && !failed) {
+          have_turn = wait_turn(ctr, rank, a.spin_limit);
+          if (!have_turn) {
+            failed = true;
+            __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          } else if (rank > 0) {
+            load_acc(q0);  // late fetch: the turn came after the early poll
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           }
         }
-        __syncthreads();  // LDS reuse by the next block
-      } else {
-        // ---- ordered reduction into the fp32 accumulator
-        const int rank = rank_of(G, i, j);
-        const bool last = rank == contributors(G, i) - 1;
-        int* ctr = ctr_head + (size_t)pb * kCtrStride;
-        const bool turn = !failed && wait_turn(ctr, rank, a.spin_limit);
-        if (!turn && !failed) {
-          failed = true;
-          __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        if (turn) {
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            const int q = q0 + 32 * qb + lc;
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-              const uint32_t off = (uint32_t)(q * D + 32 * w + 8 * rb + 4 * g);
-              f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
-              if (rank > 0) {
-                const f32x4 old = __builtin_bit_cast(f32x4, ld16_coherent(racc, off * 4));
-                v = old + v;
-              }
-              if (last) {
-                u32x2 t = {pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)};
-                st8(rdq, off * 2, t);
-                if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
-              } else {
-                st16_coherent(racc, off * 4, __builtin_bit_cast(u32x4, v));
-              }
-            }
-          }
-        }
-        // every wave's stores complete before the counter moves on
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        add = have_turn && rank > 0;
+        // every wave's view of the turn differs only on failure; a late fetch by
+        // some waves must be visible to all before the adds
         __syncthreads();
-        if (tid == 0) {
-          if (a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
-          __hip_atomic_store(ctr, rank + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      // ---- add this wave's partial into the LDS accumulator block (each element
+      //      touched by exactly one lane: a fixed, race-free order)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb) {
+          const int q = 32 * qb + lc, c = (8 * w + 2 * rb + g) ^ (q & 7);
+          f32x4* pa = (f32x4*)&sm.acc[(q * FCR + c) * 4];
+          f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+          if (add) v = *pa + v;
+          *pa = v;
+        }
+      __syncthreads();
+
+      // ---- coalesced write-back: thread owns 16-byte slots k*NT + tid
+      const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
+#pragma unroll
+      for (int k = 0; k < ALD; ++k) {
+        const int slot = k * NT + tid, r = slot / FCR, c = (slot % FCR) ^ (r & 7);
+        const f32x4 v = *(const f32x4*)&sm.acc[slot * 4];
+        const uint32_t off = (uint32_t)((q0 + r) * D + 4 * c);
+        if (!ordered) {
+          if (q0 + r < N) {
+            float* dst = a.dqacc + head + (size_t)off;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) atomicAdd(dst + e, v[e]);
+          }
+        } else if (have_turn) {
+          if (last) {
+            u32x2 t = {pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)};
+            st8(rdq, off * 2, t);
+            if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
+          } else {
+            st16_coherent(racc, off * 4, __builtin_bit_cast(u32x4, v));
+          }
         }
       }
+      if (ordered) {
+        if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
+        pend_ctr = pb;
+        pend_val = rank + 1;
+        if (!deferred || nst >= nsteps) {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          __syncthreads();
+          release();
+        }
+      }
+      buf ^= 1;
       st = nst;
     }
     if (cur_j >= 0) store_dkdv(cur_j);
