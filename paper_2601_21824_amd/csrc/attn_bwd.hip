@@ -51,7 +51,10 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a, int zero_acc) {
   // ends with the same bits and the tree is fixed
 #pragma unroll
   for (int off = 1; off < TPR; off <<= 1) acc += __shfl_xor(acc, off);
-  if (row < rows && c == 0) a.dvec[row] = acc;
+  if (row < rows && c == 0) {
+    a.dvec[row] = acc;
+    a.lse2[row] = a.lse[row] * kLog2e;
+  }
 
   const long nthreads = (long)gridDim.x * 256;
   const long nctr = (long)a.bh * a.nblk;
@@ -111,6 +114,12 @@ __device__ inline int f_at(int r, int col) {  // element index in a [rows][D] fp
   return r * D + (((col >> 2) ^ (r & 7)) << 2);
 }
 
+// dS^T tile [kv][64 q] bf16: 8-byte slot s of row r lives at s ^ swt(r), so
+// 16-lane 8-byte writes down a column and transposed reads of 4 rows are both
+// bank-conflict free.
+__device__ inline int swt(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ inline int dst_at(int r, int q) { return r * kBlockRows + (((q >> 2) ^ swt(r)) << 2); }
+
 // 4 bf16 of one column from 4 consecutive rows (gfx950 transpose read): within
 // each group of 16 lanes, lane L addresses row L/4, columns 4*(L%4)..+3 of a
 // 4 x 16 tile and receives column L of it.
@@ -139,14 +148,14 @@ struct MainSmem {
   __bf16 ks[D * D];        // K tile [kv][d] (BC = D rows)
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
-  __bf16 dss[BM * D];      // dS (bf16) [q][kv]
+  __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], 8-byte slot s of row r at s ^ swt(r)
   float acc[BM * D];       // dQ accumulator block [q][d] fp32 (chunk c at c ^ (q & 7))
-  float ls[2][BM];         // L per query row
+  float ls[2][BM];         // L * log2(e) per query row
   float ds[2][BM];         // D per query row
   int item;
 };
 
-template <int D>
+template <int D, bool CAUSAL>
 __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   constexpr int NW = D / 32;    // waves
   constexpr int NT = 64 * NW;   // threads
@@ -217,7 +226,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         lds_load16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
         lds_load16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
       }
-      if (w == 0) lds_load4(make_rsrc(a.lse + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(q0 + l) * 4);
+      if (w == 0) lds_load4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(q0 + l) * 4);
       if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(q0 + l) * 4);
     };
     // fp32 accumulator block of rows q0.. into sm.acc (device-coherent loads)
@@ -337,13 +346,17 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         }
       }
 
-      // ---- P = exp(S - L), dS = P (dP - D); element (qb, r) is query
-      //      q0 + 32qb + 8(r/4) + 4g + r%4, key j*BC + 32w + lc
-      const int kv = j * BC + 32 * w + lc;
-      const bool need_mask = (j * BC + BC > N) || (G.causal && j * BC + BC - 1 > q0);
-      bf16x8 pbf[2][2], dsbf[2][2];
+      // ---- per 32-query half: P = exp(S - L), dS = P (dP - D), then
+      //      dV += P^T dO and dK += dS^T Q (A operands straight from registers,
+      //      B operands by transposed reads of the row-major Q / dO tiles), and
+      //      dS^T -> LDS.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of
+      //      the block and key 32w + lc of the tile.  Keys past N need no mask:
+      //      their K, V rows read as zero and their dK, dV rows are not stored.
+      const int kvl = 32 * w + lc;
+      const int thr = j * BC + kvl - q0 - 4 * g;  // causal: masked iff 32qb+8rb+c < thr
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
+        bf16x8 pbf[2], dsbf[2];
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
           const int ql = 32 * qb + 8 * rb + 4 * g;
@@ -352,45 +365,36 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const int r = 4 * rb + c;
-            float p = exp2f(__builtin_fmaf(s[qb][r], c2, -L4[c] * kLog2e));
-            if (need_mask) {
-              const int qg = q0 + ql + c;
-              if (kv >= N || (G.causal && kv > qg)) p = 0.f;
-            }
+            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, -L4[c]));
+            if (CAUSAL) p = (32 * qb + 8 * rb + c < thr) ? 0.f : p;
             s[qb][r] = p;
             dp[qb][r] = p * (dp[qb][r] - D4[c]);
           }
         }
-        pbf[qb][0] = pack8(s[qb], 0);
-        pbf[qb][1] = pack8(s[qb], 8);
-        dsbf[qb][0] = pack8(dp[qb], 0);
-        dsbf[qb][1] = pack8(dp[qb], 8);
-      }
-
-      // ---- dV += P^T dO, dK += dS^T Q: A operands from registers, B operands
-      //      by transposed reads of the row-major Q / dO tiles
+        pbf[0] = pack8(s[qb], 0);
+        pbf[1] = pack8(s[qb], 8);
+        dsbf[0] = pack8(dp[qb], 0);
+        dsbf[1] = pack8(dp[qb], 8);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int col = 32 * nb + 16 * nh + 4 * (L16 & 3);
+        for (int half = 0; half < 2; ++half) {
+          const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[half]);
+          *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 4 * g)] = u32x2{dv4[0], dv4[1]};
+          *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 8 + 4 * g)] = u32x2{dv4[2], dv4[3]};
+        }
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int qb = kk >> 1, half = kk & 1;
-          const int row = 32 * qb + 16 * half + 4 * g + (L16 >> 2);
-          const bf16x8 bo = as_bf16x8(tr_read(&dos[bf_at<D>(row, col)]), tr_read(&dos[bf_at<D>(row + 8, col)]));
-          const bf16x8 bq = as_bf16x8(tr_read(&qs[bf_at<D>(row, col)]), tr_read(&qs[bf_at<D>(row + 8, col)]));
-          dvacc[nb] = mfma32(pbf[qb][half], bo, dvacc[nb]);
-          dkacc[nb] = mfma32(dsbf[qb][half], bq, dkacc[nb]);
+        for (int nb = 0; nb < NB; ++nb) {
+          const int col = 32 * nb + 16 * nh + 4 * (L16 & 3);
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int row = 32 * qb + 16 * half + 4 * g + (L16 >> 2);
+            const bf16x8 bo = as_bf16x8(tr_read(&dos[bf_at<D>(row, col)]), tr_read(&dos[bf_at<D>(row + 8, col)]));
+            const bf16x8 bq = as_bf16x8(tr_read(&qs[bf_at<D>(row, col)]), tr_read(&qs[bf_at<D>(row + 8, col)]));
+            dvacc[nb] = mfma32(pbf[half], bo, dvacc[nb]);
+            dkacc[nb] = mfma32(dsbf[half], bq, dkacc[nb]);
+          }
         }
       }
 
-      // ---- dS -> LDS as [q][kv] for the dQ product
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ql = 32 * qb + 8 * (r >> 2) + 4 * g + (r & 3);
-          sm.dss[bf_at<D>(ql, 32 * w + lc)] = (__bf16)dp[qb][r];
-        }
       // previous block's accumulator stores (deferred release) and this block's
       // early accumulator fetch are complete
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -410,7 +414,8 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         const bf16x8 ak = as_bf16x8(tr_read(&sm.ks[bf_at<D>(krow, kcol)]), tr_read(&sm.ks[bf_at<D>(krow + 4, kcol)]));
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-          const bf16x8 bs = *(const bf16x8*)&sm.dss[bf_at<D>(32 * qb + lc, 16 * ks + 8 * g)];
+          const int qc = 32 * qb + 16 * nh + 4 * (L16 & 3);
+          const bf16x8 bs = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc)]), tr_read(&sm.dst[dst_at(krow + 4, qc)]));
           dq[qb] = mfma32(ak, bs, dq[qb]);
         }
       }
@@ -508,13 +513,19 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
   if (d == 64) {
     hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
-    hipLaunchKernelGGL(bwd_main_kernel<64>, dim3(grid_main), dim3(128), 0, stream, a);
+    if (a.G.causal)
+      hipLaunchKernelGGL((bwd_main_kernel<64, true>), dim3(grid_main), dim3(128), 0, stream, a);
+    else
+      hipLaunchKernelGGL((bwd_main_kernel<64, false>), dim3(grid_main), dim3(128), 0, stream, a);
     if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
     if (atomic) hipLaunchKernelGGL(bwd_post_kernel<64>, dim3(1024), dim3(256), 0, stream, a);
   } else {
     hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
     if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
-    hipLaunchKernelGGL(bwd_main_kernel<128>, dim3(grid_main), dim3(256), 0, stream, a);
+    if (a.G.causal)
+      hipLaunchKernelGGL((bwd_main_kernel<128, true>), dim3(grid_main), dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((bwd_main_kernel<128, false>), dim3(grid_main), dim3(256), 0, stream, a);
     if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
     if (atomic) hipLaunchKernelGGL(bwd_post_kernel<128>, dim3(1024), dim3(256), 0, stream, a);
   }
@@ -523,10 +534,12 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 
 int bwd_main_occupancy(int d) {
   int blocks = 0;
-  hipError_t e = d == 64
-                     ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<64>, 128, 0)
-                     : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<128>, 256, 0);
-  return e == hipSuccess ? blocks : 0;
+  int b2 = 0;
+  hipError_t e = d == 64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<64, false>, 128, 0)
+                         : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<128, false>, 256, 0);
+  hipError_t e2 = d == 64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&b2, bwd_main_kernel<64, true>, 128, 0)
+                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&b2, bwd_main_kernel<128, true>, 256, 0);
+  return (e == hipSuccess && e2 == hipSuccess) ? (blocks < b2 ? blocks : b2) : 0;
 }
 
 }  // namespace dash

@@ -28,7 +28,7 @@ int hip_fail(hipError_t e, const char* what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctrl, dqacc, dvec, counters, total;
+  size_t ctrl, dqacc, dvec, lse2, counters, total;
 };
 
 // ctrl first so that dash_bwd_check can find it without the problem size
@@ -42,6 +42,8 @@ Layout layout(int B, int H, int N, int d) {
   L.dqacc = off;
   off += align256(bh * N * d * sizeof(float));
   L.dvec = off;
+  off += align256(bh * N * sizeof(float));
+  L.lse2 = off;
   off += align256(bh * N * sizeof(float));
   L.counters = off;
   off += align256(bh * nblk * dash::kCtrStride * sizeof(int));
@@ -199,6 +201,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   a.dv = dv;
   a.dqacc = (float*)(ws + L.dqacc);
   a.dvec = (float*)(ws + L.dvec);
+  a.lse2 = (float*)(ws + L.lse2);
   a.counters = (int*)(ws + L.counters);
   a.ctrl = (int*)(ws + L.ctrl);
   a.witness = opts ? opts->witness : nullptr;

@@ -35,6 +35,7 @@ struct BwdArgs {
   void* dv;
   float* dqacc;   // [bh][N][d] fp32 accumulator
   float* dvec;    // [bh][N] D = rowsum(dO o O)
+  float* lse2;    // [bh][N] L * log2(e)
   int* counters;  // [bh][nblk] ordering counters, kCtrStride ints apart
   int* ctrl;      // ticket / error flag
   int32_t* witness;
