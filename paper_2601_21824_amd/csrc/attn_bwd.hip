@@ -142,10 +142,24 @@ __device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t o
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
 }
 
+// Scheduling hints (one wave per SIMD, so latency must be hidden inside the
+// wave): keep `AHEAD` LDS reads in flight ahead of a run of N MFMAs, then
+// issue PER reads and VALU_PER vector ops after each MFMA.
+template <int N, int AHEAD, int PER, int VALU_PER>
+__device__ inline void sched_mfma_pipeline() {
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (PER) __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);
+    if (VALU_PER) __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0);
+  }
+}
+
 template <int D>
 struct MainSmem {
   static constexpr int BM = kBlockRows;
-  __bf16 ks[D * D];        // K tile [kv][d] (BC = D rows)
+  __bf16 vs[D * D];        // V tile [kv][d] (BC = D rows)
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
   __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], 8-byte slot s of row r at s ^ swt(r)
@@ -203,7 +217,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 
     const int nsteps = chain_len(G, wch) * G.nsub;
     int cur_j = -1;
-    bf16x8 kreg[KS], vreg[KS];
+    bf16x8 kreg[KS], ktreg[KSC];  // K rows (B of S = Q K^T), K^T (A of dQ^T = K^T dS^T)
     f32x16 dkacc[NB], dvacc[NB];
     int pend_ctr = -1, pend_val = 0;  // deferred counter release
 
@@ -278,17 +292,22 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         const int kv0 = j * BC;
         const int kvr = kv0 + 32 * w + lc;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const uint32_t off = (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2;
-          kreg[ks] = as_bf16x8(ld16(rk, off));
-          vreg[ks] = as_bf16x8(ld16(rv, off));
+        for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(rk, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
+        // K^T operand: lane holds column d = 32w + lc of K over keys 16ks + 8g .. +7
+#pragma unroll
+        for (int ks = 0; ks < KSC; ++ks) {
+          unsigned short t[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) t[e] = ld2(rk, (uint32_t)((kv0 + 16 * ks + 8 * g + e) * D + 32 * w + lc) * 2);
+          ktreg[ks] = as_bf16x8(u32x4{t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16),
+                                      t[4] | ((unsigned)t[5] << 16), t[6] | ((unsigned)t[7] << 16)});
         }
-        // K tile into LDS for the transposed (K^T) operand of the dQ product;
-        // the previous tile's readers all passed the last barrier
+        // V tile into LDS (B operand of dP = dO V^T); the previous tile's
+        // readers all passed the last barrier
 #pragma unroll
         for (int k = 0; k < KLD; ++k) {
           const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
-          lds_load16(rk, &sm.ks[(k * NT + 64 * w) * 8], (uint32_t)((kv0 + r) * D + 8 * c) * 2);
+          lds_load16(rv, &sm.vs[(k * NT + 64 * w) * 8], (uint32_t)((kv0 + r) * D + 8 * c) * 2);
         }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
@@ -329,34 +348,50 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 
       const __bf16* qs = sm.qs[buf];
       const __bf16* dos = sm.dos[buf];
-      // ---- S = Q K^T and dP = dO V^T for this wave's 32 KV columns
+      // ---- S = Q K^T and dP = dO V^T for this wave's 32 KV columns.  Software
+      //      pipelined by hand: operand i (k-step i/4, query half (i/2)%2, Q or
+      //      dO by i%2) is read RING reads ahead of its MFMA; the fences keep
+      //      that issue order, so LDS latency hides behind earlier MFMAs.
       f32x16 s[2], dp[2];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           s[qb][r] = 0.f;
           dp[qb][r] = 0.f;
         }
+      {
+        // k-step ks: A = Q rows of both query halves, A = dO rows, B = V rows of
+        // this wave's keys (read once, used by both halves); next k-step's five
+        // reads are issued before this k-step's four MFMAs.
+        auto rd = [&](int ks, bf16x8* op) {
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            const int at = bf_at<D>(32 * qb + lc, 16 * ks + 8 * g);
+            op[qb] = *(const bf16x8*)&qs[at];
+            op[2 + qb] = *(const bf16x8*)&dos[at];
+          }
+          op[4] = *(const bf16x8*)&sm.vs[bf_at<D>(32 * w + lc, 16 * ks + 8 * g)];
+        };
+        bf16x8 ring[2][5];
+        rd(0, ring[0]);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const int at = bf_at<D>(32 * qb + lc, 16 * ks + 8 * g);
-          s[qb] = mfma32(*(const bf16x8*)&qs[at], kreg[ks], s[qb]);
-          dp[qb] = mfma32(*(const bf16x8*)&dos[at], vreg[ks], dp[qb]);
+          if (ks + 1 < KS) rd(ks + 1, ring[(ks + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);
+          const bf16x8* op = ring[ks & 1];
+          s[0] = mfma32(op[0], kreg[ks], s[0]);
+          dp[0] = mfma32(op[2], op[4], dp[0]);
+          s[1] = mfma32(op[1], kreg[ks], s[1]);
+          dp[1] = mfma32(op[3], op[4], dp[1]);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
 
-      // ---- per 32-query half: P = exp(S - L), dS = P (dP - D), then
-      //      dV += P^T dO and dK += dS^T Q (A operands straight from registers,
-      //      B operands by transposed reads of the row-major Q / dO tiles), and
-      //      dS^T -> LDS.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of
-      //      the block and key 32w + lc of the tile.  Keys past N need no mask:
-      //      their K, V rows read as zero and their dK, dV rows are not stored.
       const int kvl = 32 * w + lc;
       const int thr = j * BC + kvl - q0 - 4 * g;  // causal: masked iff 32qb+8rb+c < thr
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        bf16x8 pbf[2], dsbf[2];
+      bf16x8 pbf[2][2], dsbf[2][2];
+      auto softmax_grad = [&](int qb) {
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
           const int ql = 32 * qb + 8 * rb + 4 * g;
@@ -371,29 +406,55 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
             dp[qb][r] = p * (dp[qb][r] - D4[c]);
           }
         }
-        pbf[0] = pack8(s[qb], 0);
-        pbf[1] = pack8(s[qb], 8);
-        dsbf[0] = pack8(dp[qb], 0);
-        dsbf[1] = pack8(dp[qb], 8);
+        pbf[qb][0] = pack8(s[qb], 0);
+        pbf[qb][1] = pack8(s[qb], 8);
+        dsbf[qb][0] = pack8(dp[qb], 0);
+        dsbf[qb][1] = pack8(dp[qb], 8);
+      };
+      auto store_ds = [&](int qb) {
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[half]);
+          const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[qb][half]);
           *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 4 * g)] = u32x2{dv4[0], dv4[1]};
           *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 8 + 4 * g)] = u32x2{dv4[2], dv4[3]};
         }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
+      };
+      auto dvdk = [&](int qb) {
+        // operand pair k = (nb, half) = (k / 2, k % 2): B of dV (dO^T) and of dK (Q^T)
+        constexpr int NP = 2 * NB, RING = 3;
+        auto rd = [&](int k, bf16x8* bo, bf16x8* bq) {
+          const int nb = k >> 1, half = k & 1;
           const int col = 32 * nb + 16 * nh + 4 * (L16 & 3);
+          const int row = 32 * qb + 16 * half + 4 * g + (L16 >> 2);
+          *bo = as_bf16x8(tr_read(&dos[bf_at<D>(row, col)]), tr_read(&dos[bf_at<D>(row + 8, col)]));
+          *bq = as_bf16x8(tr_read(&qs[bf_at<D>(row, col)]), tr_read(&qs[bf_at<D>(row + 8, col)]));
+        };
+        bf16x8 ro[RING], rq[RING];
 #pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            const int row = 32 * qb + 16 * half + 4 * g + (L16 >> 2);
-            const bf16x8 bo = as_bf16x8(tr_read(&dos[bf_at<D>(row, col)]), tr_read(&dos[bf_at<D>(row + 8, col)]));
-            const bf16x8 bq = as_bf16x8(tr_read(&qs[bf_at<D>(row, col)]), tr_read(&qs[bf_at<D>(row + 8, col)]));
-            dvacc[nb] = mfma32(pbf[half], bo, dvacc[nb]);
-            dkacc[nb] = mfma32(dsbf[half], bq, dkacc[nb]);
-          }
+        for (int k = 0; k < RING; ++k) rd(k, &ro[k], &rq[k]);
+#pragma unroll
+        for (int k = 0; k < NP; ++k) {
+          __builtin_amdgcn_sched_barrier(0);
+          const int nb = k >> 1, half = k & 1;
+          dvacc[nb] = mfma32(pbf[qb][half], ro[k % RING], dvacc[nb]);
+          dkacc[nb] = mfma32(dsbf[qb][half], rq[k % RING], dkacc[nb]);
+          if (k + RING < NP) rd(k + RING, &ro[k % RING], &rq[k % RING]);
         }
-      }
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // ---- per 32-query half: P = exp(S - L), dS = P (dP - D), then
+      //      dV += P^T dO and dK += dS^T Q (A operands straight from registers,
+      //      B operands by transposed reads of the row-major Q / dO tiles), and
+      //      dS^T -> LDS.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of
+      //      the block and key 32w + lc of the tile.  Keys past N need no mask:
+      //      their K, V rows read as zero and their dK, dV rows are not stored.
+      //      The second half's exp work is interleaved with the first half's MFMAs.
+      softmax_grad(0);
+      store_ds(0);
+      softmax_grad(1);
+      store_ds(1);
+      dvdk(0);
+      dvdk(1);
 
       // previous block's accumulator stores (deferred release) and this block's
       // early accumulator fetch are complete
@@ -401,23 +462,32 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       __syncthreads();
       release();
 
-      // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T
+      // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T,
+      //      k-step ks reads A = K^T (shared by both query halves) and two B's
       f32x16 dq[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) dq[qb][r] = 0.f;
+      {
+        constexpr int RING = 3;
+        auto rd = [&](int ks, bf16x8* b0, bf16x8* b1) {
+          const int krow = 16 * ks + 8 * g + (L16 >> 2);
+          const int qc0 = 16 * nh + 4 * (L16 & 3), qc1 = 32 + qc0;
+          *b0 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc0)]), tr_read(&sm.dst[dst_at(krow + 4, qc0)]));
+          *b1 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc1)]), tr_read(&sm.dst[dst_at(krow + 4, qc1)]));
+        };
+        bf16x8 rb0[RING], rb1[RING];
 #pragma unroll
-      for (int ks = 0; ks < KSC; ++ks) {
-        const int krow = 16 * ks + 8 * g + (L16 >> 2);
-        const int kcol = 32 * w + 16 * nh + 4 * (L16 & 3);
-        const bf16x8 ak = as_bf16x8(tr_read(&sm.ks[bf_at<D>(krow, kcol)]), tr_read(&sm.ks[bf_at<D>(krow + 4, kcol)]));
+        for (int k = 0; k < RING; ++k) rd(k, &rb0[k], &rb1[k]);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const int qc = 32 * qb + 16 * nh + 4 * (L16 & 3);
-          const bf16x8 bs = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc)]), tr_read(&sm.dst[dst_at(krow + 4, qc)]));
-          dq[qb] = mfma32(ak, bs, dq[qb]);
+        for (int ks = 0; ks < KSC; ++ks) {
+          __builtin_amdgcn_sched_barrier(0);
+          dq[0] = mfma32(ktreg[ks], rb0[ks % RING], dq[0]);
+          dq[1] = mfma32(ktreg[ks], rb1[ks % RING], dq[1]);
+          if (ks + RING < KSC) rd(ks + RING, &rb0[ks % RING], &rb1[ks % RING]);
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
       // dq[qb][r] <-> query 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
 
