@@ -86,6 +86,8 @@ __global__ __launch_bounds__(256) void bwd_post_kernel(BwdArgs a) {
 
 // ---------------------------------------------------------------- ordering
 // Spin until *ctr == want (relaxed, device-coherent loads).  Wave-uniform.
+// A block's counter advances by one per wave of each contributor, so rank r
+// holds the turn when it reads (waves per workgroup) * r.
 // Returns false after `limit` polls; the caller then skips its update.
 __device__ inline bool wait_turn(const int* ctr, int want, int limit) {
   for (int n = 0;; ++n) {
@@ -156,6 +158,14 @@ __device__ inline void sched_mfma_pipeline() {
   }
 }
 
+// One step of a chain, packed for the LDS step table: 64-row block pb (12
+// bits), KV tile j (9), rank in the block's summation order (10), last (1).
+// kNoStep marks a step whose block or KV tile lies past N.
+constexpr unsigned kNoStep = 0xffffffffu;
+__device__ inline unsigned pack_step(int pb, int j, int rank, bool last) {
+  return (unsigned)pb | ((unsigned)j << 12) | ((unsigned)rank << 21) | ((unsigned)last << 31);
+}
+
 template <int D>
 struct MainSmem {
   static constexpr int BM = kBlockRows;
@@ -163,9 +173,10 @@ struct MainSmem {
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
   __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], 8-byte slot s of row r at s ^ swt(r)
-  float acc[BM * D];       // dQ accumulator block [q][d] fp32 (chunk c at c ^ (q & 7))
+  float acc[BM * D];       // dQ accumulator block: wave w's columns [32w, 32w+32) as [q][8 chunks], chunk c at c ^ (q & 7)
   float ls[2][BM];         // L * log2(e) per query row
   float ds[2][BM];         // D per query row
+  unsigned steps[kMaxChainSteps];  // this chain's blocks, see pack_step
   int item;
 };
 
@@ -216,19 +227,27 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
 
     const int nsteps = chain_len(G, wch) * G.nsub;
+    // the chain's schedule, computed once into LDS (the previous chain's
+    // readers all passed the barrier after the ticket)
+    for (int st = tid; st < nsteps; st += NT) {
+      int j, i;
+      task(G, wch, st / G.nsub, &j, &i);
+      const int pb = i * G.nsub + st % G.nsub;
+      sm.steps[st] = (pb * BM < N && j * BC < N) ? pack_step(pb, j, rank_of(G, i, j), rank_of(G, i, j) == contributors(G, i) - 1)
+                                                 : kNoStep;
+    }
+    __syncthreads();
     int cur_j = -1;
     bf16x8 kreg[KS], ktreg[KSC];  // K rows (B of S = Q K^T), K^T (A of dQ^T = K^T dS^T)
     f32x16 dkacc[NB], dvacc[NB];
-    int pend_ctr = -1, pend_val = 0;  // deferred counter release
+    int pend_ctr = -1;  // block whose counter this wave still has to advance
+    int poll_v = -1;    // counter value of the coming block, loaded one step early
+    bool top_wait = true;  // first block / new V tile: wait for this wave's LDS loads at the top
 
-    auto step_block = [&](int st, int* j, int* i, int* pb) {
-      task(G, wch, st / G.nsub, j, i);
-      *pb = *i * G.nsub + st % G.nsub;
-    };
-    auto valid_step = [&](int st) {
-      int j, i, pb;
-      step_block(st, &j, &i, &pb);
-      return pb * BM < N && j * BC < N;
+    auto step_at = [&](int st) -> unsigned { return __builtin_amdgcn_readfirstlane(sm.steps[st]); };
+    auto next_valid = [&](int st) {
+      while (st < nsteps && step_at(st) == kNoStep) ++st;
+      return st;
     };
     // Q / dO / L / D of block pb into LDS buffer b (asynchronous, vmcnt)
     auto load_block = [&](int pb, int b) {
@@ -243,13 +262,16 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       if (w == 0) lds_load4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(q0 + l) * 4);
       if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(q0 + l) * 4);
     };
-    // fp32 accumulator block of rows q0.. into sm.acc (device-coherent loads)
+    // This wave's slice of the fp32 accumulator block (rows q0..q0+63,
+    // columns [32w, 32w+32)) into its LDS region, device-coherent loads.
+    // Lane l of step k covers row 8k + l/8 and physical chunk l%8.
+    float* acc_w = &sm.acc[w * BM * 32];
+    auto slot_row = [&](int k) { return 8 * k + (l >> 3); };
+    auto slot_col = [&](int k) { return 32 * w + 4 * ((l & 7) ^ (slot_row(k) & 7)); };
     auto load_acc = [&](int q0) {
 #pragma unroll
-      for (int k = 0; k < ALD; ++k) {
-        const int slot = k * NT + tid, r = slot / FCR, c = (slot % FCR) ^ (r & 7);
-        lds_load16_coherent(racc, &sm.acc[(k * NT + 64 * w) * 4], (uint32_t)((q0 + r) * D + 4 * c) * 4);
-      }
+      for (int k = 0; k < 8; ++k)
+        lds_load16_coherent(racc, &acc_w[k * 256], (uint32_t)((q0 + slot_row(k)) * D + slot_col(k)) * 4);
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -265,25 +287,26 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           st2(rdk, off, to_bf16(dkacc[nb][r] * a.scale));
         }
     };
-    auto release = [&]() {  // all waves' accumulator stores are complete: advance the order
-      if (tid == 0 && pend_ctr >= 0)
-        __hip_atomic_store(ctr_head + (size_t)pend_ctr * kCtrStride, pend_val, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+    // this wave's accumulator stores are complete (caller waited on vmcnt):
+    // add its share to the block's counter
+    auto release = [&]() {
+      if (l == 0 && pend_ctr >= 0)
+        __hip_atomic_fetch_add(ctr_head + (size_t)pend_ctr * kCtrStride, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       pend_ctr = -1;
     };
 
-    int st = 0;
-    while (st < nsteps && !valid_step(st)) ++st;
+    int st = next_valid(0);
     int buf = 0;
     if (st < nsteps) {
-      int j0, i0, pb0;
-      step_block(st, &j0, &i0, &pb0);
+      const int pb0 = step_at(st) & 0xfff;
       load_block(pb0, buf);
+      if (ordered) poll_v = __hip_atomic_load(ctr_head + (size_t)pb0 * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
     for (; st < nsteps;) {
-      int j, i, pb;
-      step_block(st, &j, &i, &pb);
+      const unsigned e = step_at(st);
+      const int pb = e & 0xfff, j = (e >> 12) & 0x1ff, rank = (e >> 21) & 0x3ff;
+      const bool last = (e >> 31) != 0;
       const int q0 = pb * BM;
 
       if (j != cur_j) {  // new KV tile: flush the previous one, load K/V operands
@@ -302,6 +325,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           ktreg[ks] = as_bf16x8(u32x4{t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16),
                                       t[4] | ((unsigned)t[5] << 16), t[6] | ((unsigned)t[7] << 16)});
         }
+        top_wait = true;
         // V tile into LDS (B operand of dP = dO V^T); the previous tile's
         // readers all passed the last barrier
 #pragma unroll
@@ -318,33 +342,21 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           }
       }
 
-      // ---- this block's Q / dO (and K) landed in LDS; the other buffer is free
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // ---- this block's Q / dO landed in LDS (each wave waited for its own
+      //      loads at the end of the previous block; only a new chain or V tile
+      //      waits here), so after the barrier all of it is visible and the other
+      //      buffer is free
+      if (top_wait) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      top_wait = false;
       __syncthreads();
 
       // ---- prefetch the next valid block into the other buffer
-      int nst = st + 1;
-      while (nst < nsteps && !valid_step(nst)) ++nst;
-      if (nst < nsteps) {
-        int jn, in_, pbn;
-        step_block(nst, &jn, &in_, &pbn);
-        load_block(pbn, buf ^ 1);
-      }
+      const int nst = next_valid(st + 1);
+      const int pb_next = nst < nsteps ? (int)(step_at(nst) & 0xfff) : -1;
+      if (pb_next >= 0) load_block(pb_next, buf ^ 1);
 
-      // ---- ordering: poll early; if the turn is already ours, fetch the
-      //      accumulator now so its latency hides behind this block's MFMAs
-      const int rank = rank_of(G, i, j);
-      const bool last = rank == contributors(G, i) - 1;
       int* ctr = ctr_head + (size_t)pb * kCtrStride;
       bool have_turn = false;
-      if (ordered && !failed) {
-        const int v0 = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        if (v0 == rank) {
-          have_turn = true;
-          __atomic_signal_fence(__ATOMIC_SEQ_CST);
-          if (rank > 0) load_acc(q0);
-        }
-      }
 
       const __bf16* qs = sm.qs[buf];
       const __bf16* dos = sm.dos[buf];
@@ -385,6 +397,18 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           s[1] = mfma32(op[1], kreg[ks], s[1]);
           dp[1] = mfma32(op[3], op[4], dp[1]);
           __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+
+      // ---- ordering: the counter of this block was loaded at the end of the
+      //      previous step; if the turn is ours, fetch the accumulator slice now
+      //      so that its latency hides behind the remaining MFMAs
+      if (ordered && !failed) {
+        const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
+        if (v0 == NW * rank) {
+          have_turn = true;
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+          if (rank > 0) load_acc(q0);
         }
       }
 
@@ -456,11 +480,15 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       dvdk(0);
       dvdk(1);
 
-      // previous block's accumulator stores (deferred release) and this block's
-      // early accumulator fetch are complete
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // deferred release of the previous block: its accumulator stores were
+      // followed by at least 9 vector memory operations (the counter poll and
+      // this block's Q / dO loads), and these complete in issue order, so at
+      // most 8 outstanding means the stores are done
+      if (pend_ctr >= 0) {
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        release();
+      }
       __syncthreads();
-      release();
 
       // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T,
       //      k-step ks reads A = K^T (shared by both query halves) and two B's
@@ -501,44 +529,48 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
                  __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
       }
 
-      bool add = false;  // accumulate into sm.acc (else: store the partial there)
+      bool add = false;  // accumulate into the slice (else: the partial is stored as is)
       if (ordered) {
         if (!have_turn && !failed) {
-          have_turn = wait_turn(ctr, rank, a.spin_limit);
+          have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
           if (!have_turn) {
             failed = true;
             __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           } else if (rank > 0) {
             load_acc(q0);  // late fetch: the turn came after the early poll
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           }
         }
         add = have_turn && rank > 0;
-        // every wave's view of the turn differs only on failure; a late fetch by
-        // some waves must be visible to all before the adds
-        __syncthreads();
       }
-      // ---- add this wave's partial into the LDS accumulator block (each element
-      //      touched by exactly one lane: a fixed, race-free order)
+      // this wave's slice (and the next block's Q / dO) have landed
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // ---- add this wave's partial into its slice (each element touched by
+      //      exactly one lane, so the order of the sum is fixed), then write the
+      //      slice back coalesced: all of it stays within this wave
+      {
+        f32x4 old[8];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          const int q = 32 * qb + lc, c = (8 * w + 2 * rb + g) ^ (q & 7);
-          f32x4* pa = (f32x4*)&sm.acc[(q * FCR + c) * 4];
-          f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
-          if (add) v = *pa + v;
-          *pa = v;
+        for (int k = 0; k < 8; ++k) {
+          const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
+          old[k] = *(const f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4];
         }
-      __syncthreads();
-
-      // ---- coalesced write-back: thread owns 16-byte slots k*NT + tid
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
+          f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+          const f32x4 sum = old[k] + v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
+          *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] = v;
+        }
+      }
+      asm volatile("" ::: "memory");
       const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
 #pragma unroll
-      for (int k = 0; k < ALD; ++k) {
-        const int slot = k * NT + tid, r = slot / FCR, c = (slot % FCR) ^ (r & 7);
-        const f32x4 v = *(const f32x4*)&sm.acc[slot * 4];
-        const uint32_t off = (uint32_t)((q0 + r) * D + 4 * c);
+      for (int k = 0; k < 8; ++k) {
+        const f32x4 v = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+        const int r = slot_row(k);
+        const uint32_t off = (uint32_t)((q0 + r) * D + slot_col(k));
         if (!ordered) {
           if (q0 + r < N) {
             float* dst = a.dqacc + head + (size_t)off;
@@ -558,13 +590,13 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       if (ordered) {
         if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
         pend_ctr = pb;
-        pend_val = rank + 1;
         if (!deferred || nst >= nsteps) {
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-          __syncthreads();
           release();
         }
       }
+      if (ordered && pb_next >= 0)
+        poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       buf ^= 1;
       st = nst;
     }

@@ -185,6 +185,8 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   // any other chain of its head (persistent grid, in-order work tickets).
   if (sched != DASH_SCHED_ATOMIC && G.chains > resident)
     return fail(DASH_ERR_UNSUPPORTED, "too many KV tiles per head for the resident workgroups of this GPU");
+  if ((long)(G.t_r + 1) * G.nsub > dash::kMaxChainSteps || N > 32768)
+    return fail(DASH_ERR_UNSUPPORTED, "sequence too long for one workgroup chain (N <= 32768)");
   const long items = (long)B * H * G.chains;
   const int grid = (int)(items < resident ? items : resident);
 

@@ -12,6 +12,7 @@ constexpr int kPoison = 0x40000000;   // counter start value no rank waits for
 constexpr int kCtrlTicket = 0;        // ctrl[] slot: next work item
 constexpr int kCtrlError = 16;        // ctrl[] slot: set to 1 when a wait timed out
 constexpr size_t kCtrlBytes = 256;    // ctrl block at the start of the workspace
+constexpr int kMaxChainSteps = 1040;  // 64-row blocks one workgroup chain may visit
 
 struct FwdArgs {
   const void* q;
