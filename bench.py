@@ -75,6 +75,24 @@ def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
     return wall * 1e3 / steps, sum(main_ms) / len(main_ms)
 
 
+def measured_traffic():
+    """HBM bytes per launch of the main kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None if the kernel source changed since
+    the counters were taken."""
+    import hashlib
+    summary = os.path.join(ROOT, "profiles", "bwd_main_b2h16n8192d128_full.md")
+    src = os.path.join(ROOT, "paper_2601_21824_amd", "csrc", "attn_bwd.hip")
+    try:
+        text = open(summary).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
+    if fields.get("source_sha256_prefix", "").strip() != sha:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(q, k, v, do, causal, flops_per_head):
     """The oracle, as it is, on one full head (b=0, h=0) of the workload."""
     import oracle
@@ -97,6 +115,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--N", type=int, default=8192)
     ap.add_argument("--causal", action="store_true")
+    ap.add_argument("--schedules", default="",
+                    help="comma list of schedules to time (default: the schedule, atomic, naive)")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run 5 plain device copies of this many bytes (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the backward shards over heads with no communication, "
@@ -104,6 +126,15 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_bytes:
+        src = torch.empty(args.copy_bytes, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_bytes, "copies": 5}))
+        return
 
     from paper_2601_21824_amd import binding as dash
     from paper_2601_21824_amd.synth import make_inputs
@@ -124,12 +155,17 @@ def main():
 
     results = {}
     det = args.schedule
-    for sched in dict.fromkeys([det, "atomic", "naive"]):
+    scheds = [x for x in args.schedules.split(",") if x] or [det, "atomic", "naive"]
+    for sched in dict.fromkeys(scheds):
         ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
         results[sched] = (ms, main_ms, flops / (ms * 1e-3) / 1e12)
         print(f"[bench] {sched}: {ms:.3f} ms/step, main kernel {main_ms:.3f} ms, "
               f"{results[sched][2]:.1f} TFLOPS", file=sys.stderr, flush=True)
 
+    if det not in results or "atomic" not in results:
+        print(json.dumps({s: {"ms_per_step": r[0], "main_kernel_ms": r[1], "tflops": r[2]}
+                          for s, r in results.items()}), flush=True)
+        return
     ms, main_ms, tflops = results[det]
     main_tflops = flops / (main_ms * 1e-3) / 1e12
     out = {
@@ -151,10 +187,11 @@ def main():
                    "schedule": det, "global_batch": B, "seq_len": N},
         "pct_of_atomic": round(100.0 * tflops / results["atomic"][2], 2),
         "atomic_tflops": round(results["atomic"][2], 2),
-        "naive_tflops": round(results["naive"][2], 2),
+        "naive_tflops": round(results["naive"][2], 2) if "naive" in results else None,
         "roofline": {"bound": "mfma", "kernel": "bwd_main_kernel<128>",
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic() if (N, causal, det) == (8192, False, "shift") else None,
                      "main_kernel_ms": round(main_ms, 4)},
     }
     if not args.no_cpu:
