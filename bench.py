@@ -106,6 +106,32 @@ def cpu_baseline(q, k, v, do, causal, flops_per_head):
                       f"{dt:.1f} s; FLOPs counted as 4*N^2*d*2.5 for that head"}
 
 
+def sweep(dash, make_inputs, args):
+    import torch
+    ev = HipEvents()
+    cases = [(16384 // n, 16, n, 128, False) for n in (512, 1024, 2048, 4096, 8192, 16384)]
+    cases += [(16384 // n, 32, n, 128, True) for n in (512, 1024, 2048, 4096, 8192, 16384)]
+    cases += [(4, 16, 1024, 64, True)]
+    for B, H, N, d, causal in cases:
+        flops = 4.0 * B * H * N * N * d * 2.5 / (2 if causal else 1)
+        q, k, v, do = make_inputs(B, H, N, d, seed=N + d)
+        qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
+        og, lseg = dash.attn_fwd(qg, kg, vg, causal)
+        dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
+        ws = dash.new_workspace(B, H, N, d)
+        tensors = (qg, kg, vg, og, dog, lseg, dq, dk, dv, ws)
+        scheds = ("descending", "symshift", "naive", "atomic") if causal else ("shift", "naive", "atomic")
+        row = {"B": B, "H": H, "N": N, "d": d, "mask": "causal" if causal else "full"}
+        for sched in scheds:
+            ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
+            row[sched] = round(flops / (ms * 1e-3) / 1e12, 1)
+        det = max(row[s] for s in scheds if s != "atomic")
+        row["best_det_pct_of_atomic"] = round(100 * det / row["atomic"], 1)
+        print(json.dumps(row), flush=True)
+        del tensors, qg, kg, vg, dog, og, lseg, dq, dk, dv, ws
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +143,9 @@ def main():
     ap.add_argument("--causal", action="store_true")
     ap.add_argument("--schedules", default="",
                     help="comma list of schedules to time (default: the schedule, atomic, naive)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time every schedule over the 16k-token sweeps (full H=16, causal H=32, d=128) and "
+                         "the B=4 H=16 N=1024 d=64 causal case; one JSON line per case")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run 5 plain device copies of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -140,6 +169,9 @@ def main():
     from paper_2601_21824_amd.synth import make_inputs
 
     dash.load()
+    if args.sweep:
+        sweep(dash, make_inputs, args)
+        return
     N, d, causal = args.N, 128, args.causal
     B = max(1, 16384 // N)
     H = 32 if causal else 16
@@ -188,7 +220,7 @@ def main():
         "pct_of_atomic": round(100.0 * tflops / results["atomic"][2], 2),
         "atomic_tflops": round(results["atomic"][2], 2),
         "naive_tflops": round(results["naive"][2], 2) if "naive" in results else None,
-        "roofline": {"bound": "mfma", "kernel": "bwd_main_kernel<128>",
+        "roofline": {"bound": "mfma", "kernel": "bwd_main_kernel<128, full mask, ordered>",
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic() if (N, causal, det) == (8192, False, "shift") else None,

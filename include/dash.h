@@ -52,8 +52,10 @@ typedef enum {
   /* Symmetric Shift (Section 3.4, causal masks): KV tiles j and T-1-j share a
      workgroup; two-phase fold.  Causal mask only. */
   DASH_SCHED_SYMSHIFT = 4,
-  /* SHIFT for full masks; DESCENDING for causal masks at d >= 128, SYMSHIFT
-     below (the paper's recommendation, Section 4.3). */
+  /* SHIFT for full masks, SYMSHIFT for causal masks at every head dim.  The
+     paper prefers DESCENDING at d >= 128 because Symmetric Shift costs
+     registers on its hardware (Section 4.3); here its schedule lives in an LDS
+     step table and it is the faster causal schedule at d = 64 and d = 128. */
   DASH_SCHED_AUTO = 5
 } dash_schedule_t;
 

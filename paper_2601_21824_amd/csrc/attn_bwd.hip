@@ -180,7 +180,7 @@ struct MainSmem {
   int item;
 };
 
-template <int D, bool CAUSAL>
+template <int D, bool CAUSAL, bool ORDERED>
 __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   constexpr int NW = D / 32;    // waves
   constexpr int NT = 64 * NW;   // threads
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   const int total = a.bh * G.chains;
-  const bool ordered = G.sched != S_ATOMIC;
+  constexpr bool ordered = ORDERED;  // false: the atomic variant
   // Shift-type orders are conflict-free: the next contributor to a block reaches
   // it at least one step later, so the counter release can wait until the next
   // step's barrier, by which time the accumulator stores have drained.
@@ -566,18 +566,23 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       }
       asm volatile("" ::: "memory");
       const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
+      if constexpr (!ordered) {
+        // atomic variant: one fp32 atomic per element, each instruction
+        // covering two whole 128-byte row segments of the slice
+        const int c = l & 31;
+#pragma unroll 8
+        for (int k = 0; k < 32; ++k) {
+          const int q = 2 * k + (l >> 5);
+          const float v = acc_w[(q * 8 + ((c >> 2) ^ (q & 7))) * 4 + (c & 3)];
+          if (q0 + q < N) atomicAdd(a.dqacc + head + (size_t)(q0 + q) * D + 32 * w + c, v);
+        }
+      }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < 8 && ordered; ++k) {
         const f32x4 v = *(const f32x4*)&acc_w[k * 256 + 4 * l];
         const int r = slot_row(k);
         const uint32_t off = (uint32_t)((q0 + r) * D + slot_col(k));
-        if (!ordered) {
-          if (q0 + r < N) {
-            float* dst = a.dqacc + head + (size_t)off;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) atomicAdd(dst + e, v[e]);
-          }
-        } else if (have_turn) {
+        if (have_turn) {
           if (last) {
             u32x2 t = {pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)};
             st8(rdq, off * 2, t);
@@ -605,43 +610,55 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   }
 }
 
-hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream) {
+template <int D>
+void launch_main(const BwdArgs& a, int grid_main, hipStream_t stream) {
   const bool atomic = a.G.sched == S_ATOMIC;
+  const dim3 grid(grid_main), block(2 * D);
+  if (a.G.causal) {
+    if (atomic) hipLaunchKernelGGL((bwd_main_kernel<D, true, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((bwd_main_kernel<D, true, true>), grid, block, 0, stream, a);
+  } else {
+    if (atomic) hipLaunchKernelGGL((bwd_main_kernel<D, false, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((bwd_main_kernel<D, false, true>), grid, block, 0, stream, a);
+  }
+}
+
+template <int D>
+void launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t stream) {
+  const bool atomic = a.G.sched == S_ATOMIC;
+  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
+  if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
+  launch_main<D>(a, grid_main, stream);
+  if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
+  if (atomic) hipLaunchKernelGGL(bwd_post_kernel<D>, dim3(1024), dim3(256), 0, stream, a);
+}
+
+hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream) {
   const long rows = (long)a.bh * a.n;
   const int tpr = d / 8;
   long pre_blocks = (rows * tpr + 255) / 256;
   if (pre_blocks < 1) pre_blocks = 1;
   if (pre_blocks > 65535L * 16) pre_blocks = 65535L * 16;
-  if (d == 64) {
-    hipLaunchKernelGGL(bwd_pre_kernel<64>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
-    if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
-    if (a.G.causal)
-      hipLaunchKernelGGL((bwd_main_kernel<64, true>), dim3(grid_main), dim3(128), 0, stream, a);
-    else
-      hipLaunchKernelGGL((bwd_main_kernel<64, false>), dim3(grid_main), dim3(128), 0, stream, a);
-    if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
-    if (atomic) hipLaunchKernelGGL(bwd_post_kernel<64>, dim3(1024), dim3(256), 0, stream, a);
-  } else {
-    hipLaunchKernelGGL(bwd_pre_kernel<128>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
-    if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
-    if (a.G.causal)
-      hipLaunchKernelGGL((bwd_main_kernel<128, true>), dim3(grid_main), dim3(256), 0, stream, a);
-    else
-      hipLaunchKernelGGL((bwd_main_kernel<128, false>), dim3(grid_main), dim3(256), 0, stream, a);
-    if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
-    if (atomic) hipLaunchKernelGGL(bwd_post_kernel<128>, dim3(1024), dim3(256), 0, stream, a);
-  }
+  if (d == 64)
+    launch_all<64>(a, pre_blocks, grid_main, stream);
+  else
+    launch_all<128>(a, pre_blocks, grid_main, stream);
   return hipGetLastError();
 }
 
-int bwd_main_occupancy(int d) {
-  int blocks = 0;
-  int b2 = 0;
-  hipError_t e = d == 64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<64, false>, 128, 0)
-                         : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, bwd_main_kernel<128, false>, 256, 0);
-  hipError_t e2 = d == 64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&b2, bwd_main_kernel<64, true>, 128, 0)
-                          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&b2, bwd_main_kernel<128, true>, 256, 0);
-  return (e == hipSuccess && e2 == hipSuccess) ? (blocks < b2 ? blocks : b2) : 0;
+template <int D>
+int main_occupancy() {
+  int lo = 1 << 30;
+  const void* fns[4] = {(const void*)bwd_main_kernel<D, false, false>, (const void*)bwd_main_kernel<D, false, true>,
+                        (const void*)bwd_main_kernel<D, true, false>, (const void*)bwd_main_kernel<D, true, true>};
+  for (const void* f : fns) {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 2 * D, 0) != hipSuccess) return 0;
+    lo = blocks < lo ? blocks : lo;
+  }
+  return lo;
 }
+
+int bwd_main_occupancy(int d) { return d == 64 ? main_occupancy<64>() : main_occupancy<128>(); }
 
 }  // namespace dash
