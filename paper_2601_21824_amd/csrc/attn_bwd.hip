@@ -223,7 +223,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
     const auto rv = make_rsrc((const __bf16*)a.v + head, hbytes);
     const auto rdo = make_rsrc((const __bf16*)a.dO + head, hbytes);
-    const auto racc = make_rsrc(a.dqacc + head, hbytes * 2);
+    const auto racc = make_rsrc(a.dqacc + (size_t)bh * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
 
     const int nsteps = chain_len(G, wch) * G.nsub;
@@ -265,13 +265,15 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     // This wave's slice of the fp32 accumulator block (rows q0..q0+63,
     // columns [32w, 32w+32)) into its LDS region, device-coherent loads.
     // Lane l of step k covers row 8k + l/8 and physical chunk l%8.
+    // The ordered variants keep dQacc in register order: 64-row block pb is
+    // BM*D floats at pb*BM*D; wave w's slice (columns [32w, 32w+32)) is the
+    // 2048 floats at w*2048, chunk k (= 4 qb + rb) of lane l at k*256 + 4l
+    // holding row 32qb + l%32, columns 32w + 8rb + 4(l/32) .. +3.
     float* acc_w = &sm.acc[w * BM * 32];
-    auto slot_row = [&](int k) { return 8 * k + (l >> 3); };
-    auto slot_col = [&](int k) { return 32 * w + 4 * ((l & 7) ^ (slot_row(k) & 7)); };
-    auto load_acc = [&](int q0) {
+    auto acc_off = [&](int pb, int k) { return (uint32_t)(pb * BM * D + w * BM * 32 + k * 256 + 4 * l) * 4; };
+    auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        lds_load16_coherent(racc, &acc_w[k * 256], (uint32_t)((q0 + slot_row(k)) * D + slot_col(k)) * 4);
+      for (int k = 0; k < 8; ++k) lds_load16_coherent(racc, &acc_w[k * 256], acc_off(pb, k));
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -408,7 +410,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         if (v0 == NW * rank) {
           have_turn = true;
           __atomic_signal_fence(__ATOMIC_SEQ_CST);
-          if (rank > 0) load_acc(q0);
+          if (rank > 0) load_acc(pb);
         }
       }
 
@@ -537,59 +539,57 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
             failed = true;
             __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           } else if (rank > 0) {
-            load_acc(q0);  // late fetch: the turn came after the early poll
+            load_acc(pb);  // late fetch: the turn came after the early poll
           }
         }
         add = have_turn && rank > 0;
       }
       // this wave's slice (and the next block's Q / dO) have landed
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      // ---- add this wave's partial into its slice (each element touched by
-      //      exactly one lane, so the order of the sum is fixed), then write the
-      //      slice back coalesced: all of it stays within this wave
-      {
-        f32x4 old[8];
+      if constexpr (ordered) {
+        // ---- add this wave's partial into its slice straight from registers:
+        //      the accumulator is stored in this wave's register order, so the
+        //      slice arrives (LDS landing pad) and leaves in 1 KB coalesced rows.
+        //      Each element is touched by exactly one lane: the sum order is the
+        //      schedule's.
+        if (have_turn) {
+          const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
+          f32x4 old[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int qb = k >> 2, rb = k & 3;
+            f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+            const f32x4 sum = old[k] + v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
+            if (last) {
+              const uint32_t off = (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g);
+              st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
+              if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
+            } else {
+              st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+            }
+          }
+        }
+      } else {
+        // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
+        //      atomic per element, each instruction covering two whole 128-byte
+        //      row segments of the row-major dQacc
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
           const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
-          old[k] = *(const f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4];
+          *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] =
+              f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
         }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
-          f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
-          const f32x4 sum = old[k] + v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
-          *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] = v;
-        }
-      }
-      asm volatile("" ::: "memory");
-      const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
-      if constexpr (!ordered) {
-        // atomic variant: one fp32 atomic per element, each instruction
-        // covering two whole 128-byte row segments of the slice
+        asm volatile("" ::: "memory");  // lanes read what other lanes wrote
         const int c = l & 31;
 #pragma unroll 8
         for (int k = 0; k < 32; ++k) {
           const int q = 2 * k + (l >> 5);
           const float v = acc_w[(q * 8 + ((c >> 2) ^ (q & 7))) * 4 + (c & 3)];
           if (q0 + q < N) atomicAdd(a.dqacc + head + (size_t)(q0 + q) * D + 32 * w + c, v);
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < 8 && ordered; ++k) {
-        const f32x4 v = *(const f32x4*)&acc_w[k * 256 + 4 * l];
-        const int r = slot_row(k);
-        const uint32_t off = (uint32_t)((q0 + r) * D + slot_col(k));
-        if (have_turn) {
-          if (last) {
-            u32x2 t = {pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)};
-            st8(rdq, off * 2, t);
-            if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
-          } else {
-            st16_coherent(racc, off * 4, __builtin_bit_cast(u32x4, v));
-          }
         }
       }
       if (ordered) {

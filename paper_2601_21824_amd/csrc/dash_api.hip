@@ -40,7 +40,7 @@ Layout layout(int B, int H, int N, int d) {
   L.ctrl = off;
   off += dash::kCtrlBytes;
   L.dqacc = off;
-  off += align256(bh * N * d * sizeof(float));
+  off += align256(bh * nblk * dash::kBlockRows * d * sizeof(float));  // >= N rows per head
   L.dvec = off;
   off += align256(bh * N * sizeof(float));
   L.lse2 = off;
