@@ -169,7 +169,6 @@ __device__ inline unsigned pack_step(int pb, int j, int rank, bool last) {
 template <int D>
 struct MainSmem {
   static constexpr int BM = kBlockRows;
-  __bf16 vs[D * D];        // V tile [kv][d] (BC = D rows)
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
   __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], 8-byte slot s of row r at s ^ swt(r)
@@ -238,11 +237,11 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     }
     __syncthreads();
     int cur_j = -1;
-    bf16x8 kreg[KS], ktreg[KSC];  // K rows (B of S = Q K^T), K^T (A of dQ^T = K^T dS^T)
+    bf16x8 kreg[KS], vreg[KS], ktreg[KSC];  // K, V rows (B of S = Q K^T, dP = dO V^T), K^T (A of dQ^T = K^T dS^T)
     f32x16 dkacc[NB], dvacc[NB];
     int pend_ctr = -1;  // block whose counter this wave still has to advance
     int poll_v = -1;    // counter value of the coming block, loaded one step early
-    bool top_wait = true;  // first block / new V tile: wait for this wave's LDS loads at the top
+    bool top_wait = true;  // first block of the chain: wait for this wave's LDS loads at the top
 
     auto step_at = [&](int st) -> unsigned { return __builtin_amdgcn_readfirstlane(sm.steps[st]); };
     auto next_valid = [&](int st) {
@@ -250,21 +249,21 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       return st;
     };
     // Q / dO / L / D of block pb into LDS buffer b (asynchronous, vmcnt)
-    auto load_block = [&](int pb, int b) {
-      const int q0 = pb * BM;
-#pragma unroll
-      for (int k = 0; k < QLD; ++k) {
-        const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
-        const uint32_t off = (uint32_t)((q0 + r) * D + 8 * c) * 2;
-        lds_load16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
-        lds_load16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
-      }
-      if (w == 0) lds_load4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(q0 + l) * 4);
-      if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(q0 + l) * 4);
+    auto load_part = [&](int pb, int b, int k) {  // part k < QLD of the Q and dO rows
+      const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
+      const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
+      lds_load16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
+      lds_load16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
     };
-    // This wave's slice of the fp32 accumulator block (rows q0..q0+63,
-    // columns [32w, 32w+32)) into its LDS region, device-coherent loads.
-    // Lane l of step k covers row 8k + l/8 and physical chunk l%8.
+    auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
+      if (w == 0) lds_load4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + l) * 4);
+      if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + l) * 4);
+    };
+    auto load_block = [&](int pb, int b) {
+#pragma unroll
+      for (int k = 0; k < QLD; ++k) load_part(pb, b, k);
+      load_ld(pb, b);
+    };
     // The ordered variants keep dQacc in register order: 64-row block pb is
     // BM*D floats at pb*BM*D; wave w's slice (columns [32w, 32w+32)) is the
     // 2048 floats at w*2048, chunk k (= 4 qb + rb) of lane l at k*256 + 4l
@@ -317,7 +316,10 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         const int kv0 = j * BC;
         const int kvr = kv0 + 32 * w + lc;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kreg[ks] = as_bf16x8(ld16(rk, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
+        for (int ks = 0; ks < KS; ++ks) {
+          kreg[ks] = as_bf16x8(ld16(rk, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
+          vreg[ks] = as_bf16x8(ld16(rv, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
+        }
         // K^T operand: lane holds column d = 32w + lc of K over keys 16ks + 8g .. +7
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks) {
@@ -326,14 +328,6 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           for (int e = 0; e < 8; ++e) t[e] = ld2(rk, (uint32_t)((kv0 + 16 * ks + 8 * g + e) * D + 32 * w + lc) * 2);
           ktreg[ks] = as_bf16x8(u32x4{t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16),
                                       t[4] | ((unsigned)t[5] << 16), t[6] | ((unsigned)t[7] << 16)});
-        }
-        top_wait = true;
-        // V tile into LDS (B operand of dP = dO V^T); the previous tile's
-        // readers all passed the last barrier
-#pragma unroll
-        for (int k = 0; k < KLD; ++k) {
-          const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
-          lds_load16(rv, &sm.vs[(k * NT + 64 * w) * 8], (uint32_t)((kv0 + r) * D + 8 * c) * 2);
         }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
@@ -352,20 +346,15 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       top_wait = false;
       __syncthreads();
 
-      // ---- prefetch the next valid block into the other buffer
+      // ---- the next valid block (prefetched into the other buffer below)
       const int nst = next_valid(st + 1);
       const int pb_next = nst < nsteps ? (int)(step_at(nst) & 0xfff) : -1;
-      if (pb_next >= 0) load_block(pb_next, buf ^ 1);
 
       int* ctr = ctr_head + (size_t)pb * kCtrStride;
       bool have_turn = false;
 
       const __bf16* qs = sm.qs[buf];
       const __bf16* dos = sm.dos[buf];
-      // ---- S = Q K^T and dP = dO V^T for this wave's 32 KV columns.  Software
-      //      pipelined by hand: operand i (k-step i/4, query half (i/2)%2, Q or
-      //      dO by i%2) is read RING reads ahead of its MFMA; the fences keep
-      //      that issue order, so LDS latency hides behind earlier MFMAs.
       f32x16 s[2], dp[2];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
@@ -374,79 +363,88 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           s[qb][r] = 0.f;
           dp[qb][r] = 0.f;
         }
-      {
-        // k-step ks: A = Q rows of both query halves, A = dO rows, B = V rows of
-        // this wave's keys (read once, used by both halves); next k-step's five
-        // reads are issued before this k-step's four MFMAs.
-        auto rd = [&](int ks, bf16x8* op) {
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            const int at = bf_at<D>(32 * qb + lc, 16 * ks + 8 * g);
-            op[qb] = *(const bf16x8*)&qs[at];
-            op[2 + qb] = *(const bf16x8*)&dos[at];
-          }
-          op[4] = *(const bf16x8*)&sm.vs[bf_at<D>(32 * w + lc, 16 * ks + 8 * g)];
+      // The step is four runs of 16 MFMAs -- S/dP of query half 0, S/dP of
+      // half 1, dV/dK of half 0, dV/dK of half 1 -- and the vector, LDS-store
+      // and DMA work of the step is cut into pieces issued between them:
+      // the next block's prefetch during the first run, softmax of half 0 and
+      // the accumulator fetch during the second, softmax of half 1 during the
+      // third, the dS^T stores during the fourth.  The sched_barrier fences
+      // keep that interleaving.
+      //
+      // S = Q K^T, dP = dO V^T for query half qb and this wave's 32 keys:
+      // A = Q / dO rows from LDS (RING - 1 k-steps ahead), B = K / V rows
+      // from registers.
+      auto sdp = [&](int qb, auto&& extra) {
+        constexpr int RING = 4;
+        bf16x8 rq[RING], ro[RING];
+        auto rd = [&](int ks) {
+          const int at = bf_at<D>(32 * qb + lc, 16 * ks + 8 * g);
+          rq[ks % RING] = *(const bf16x8*)&qs[at];
+          ro[ks % RING] = *(const bf16x8*)&dos[at];
         };
-        bf16x8 ring[2][5];
-        rd(0, ring[0]);
+#pragma unroll
+        for (int k = 0; k < RING - 1; ++k) rd(k);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          if (ks + 1 < KS) rd(ks + 1, ring[(ks + 1) & 1]);
+          if (ks + RING - 1 < KS) rd(ks + RING - 1);
           __builtin_amdgcn_sched_barrier(0);
-          const bf16x8* op = ring[ks & 1];
-          s[0] = mfma32(op[0], kreg[ks], s[0]);
-          dp[0] = mfma32(op[2], op[4], dp[0]);
-          s[1] = mfma32(op[1], kreg[ks], s[1]);
-          dp[1] = mfma32(op[3], op[4], dp[1]);
+          s[qb] = mfma32(rq[ks % RING], kreg[ks], s[qb]);
+          dp[qb] = mfma32(ro[ks % RING], vreg[ks], dp[qb]);
+          extra(ks);
           __builtin_amdgcn_sched_barrier(0);
         }
-      }
+      };
 
-      // ---- ordering: the counter of this block was loaded at the end of the
-      //      previous step; if the turn is ours, fetch the accumulator slice now
-      //      so that its latency hides behind the remaining MFMAs
-      if (ordered && !failed) {
-        const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
-        if (v0 == NW * rank) {
-          have_turn = true;
-          __atomic_signal_fence(__ATOMIC_SEQ_CST);
-          if (rank > 0) load_acc(pb);
-        }
-      }
-
+      // P = exp(S - L), dS = P (dP - D) in 8 pieces per query half: piece k
+      // covers row group rb = k/2 (queries 32qb + 8rb + 4g + c) for c in
+      // {2(k%2), 2(k%2)+1}; L and D of the next row group are read one piece
+      // ahead.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of the block
+      // and key 32w + lc of the tile.  Keys past N need no mask: their K, V
+      // rows read as zero and their dK, dV rows are not stored.
       const int kvl = 32 * w + lc;
       const int thr = j * BC + kvl - q0 - 4 * g;  // causal: masked iff 32qb+8rb+c < thr
       bf16x8 pbf[2][2], dsbf[2][2];
-      auto softmax_grad = [&](int qb) {
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          const int ql = 32 * qb + 8 * rb + 4 * g;
-          const f32x4 L4 = *(const f32x4*)&sm.ls[buf][ql];
-          const f32x4 D4 = *(const f32x4*)&sm.ds[buf][ql];
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const int r = 4 * rb + c;
-            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, -L4[c]));
-            if (CAUSAL) p = (32 * qb + 8 * rb + c < thr) ? 0.f : p;
-            s[qb][r] = p;
-            dp[qb][r] = p * (dp[qb][r] - D4[c]);
-          }
-        }
-        pbf[qb][0] = pack8(s[qb], 0);
-        pbf[qb][1] = pack8(s[qb], 8);
-        dsbf[qb][0] = pack8(dp[qb], 0);
-        dsbf[qb][1] = pack8(dp[qb], 8);
+      f32x4 Lc, Dc, Ln, Dn;
+      auto read_ld = [&](int qb, int rb) {
+        const int ql = 32 * qb + 8 * rb + 4 * g;
+        Ln = *(const f32x4*)&sm.ls[buf][ql];
+        Dn = *(const f32x4*)&sm.ds[buf][ql];
       };
-      auto store_ds = [&](int qb) {
+      auto softmax_piece = [&](int qb, int k) {
+        const int rb = k >> 1;
+        if ((k & 1) == 0) {
+          Lc = Ln;
+          Dc = Dn;
+        } else if (rb < 3 || qb == 0) {
+          read_ld(rb < 3 ? qb : qb + 1, rb < 3 ? rb + 1 : 0);
+        }
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[qb][half]);
-          *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 4 * g)] = u32x2{dv4[0], dv4[1]};
-          *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 8 + 4 * g)] = u32x2{dv4[2], dv4[3]};
+        for (int cc = 0; cc < 2; ++cc) {
+          const int c = 2 * (k & 1) + cc, r = 4 * rb + c;
+          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, -Lc[c]));
+          if (CAUSAL) p = (32 * qb + 8 * rb + c < thr) ? 0.f : p;
+          s[qb][r] = p;
+          dp[qb][r] = p * (dp[qb][r] - Dc[c]);
+        }
+        if (k == 3) {
+          pbf[qb][0] = pack8(s[qb], 0);
+          dsbf[qb][0] = pack8(dp[qb], 0);
+        } else if (k == 7) {
+          pbf[qb][1] = pack8(s[qb], 8);
+          dsbf[qb][1] = pack8(dp[qb], 8);
         }
       };
-      auto dvdk = [&](int qb) {
-        // operand pair k = (nb, half) = (k / 2, k % 2): B of dV (dO^T) and of dK (Q^T)
+      // dS^T -> LDS, piece k of 8: query half k/4, 8-byte slot k%4
+      auto store_ds_piece = [&](int k) {
+        const int qb = k >> 2, half = (k >> 1) & 1, part = k & 1;
+        const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[qb][half]);
+        *(u32x2*)&sm.dst[dst_at(kvl, 32 * qb + 16 * half + 8 * part + 4 * g)] =
+            part ? u32x2{dv4[2], dv4[3]} : u32x2{dv4[0], dv4[1]};
+      };
+      // dV += P^T dO and dK += dS^T Q for query half qb: A = P^T, dS^T from
+      // registers, B = dO^T, Q^T by transposed reads of the row-major tiles
+      // (RING - 1 operand pairs ahead)
+      auto dvdk = [&](int qb, auto&& extra) {
         constexpr int NP = 2 * NB, RING = 3;
         auto rd = [&](int k, bf16x8* bo, bf16x8* bq) {
           const int nb = k >> 1, half = k & 1;
@@ -465,29 +463,58 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           dvacc[nb] = mfma32(pbf[qb][half], ro[k % RING], dvacc[nb]);
           dkacc[nb] = mfma32(dsbf[qb][half], rq[k % RING], dkacc[nb]);
           if (k + RING < NP) rd(k + RING, &ro[k % RING], &rq[k % RING]);
+          extra(k);
         }
         __builtin_amdgcn_sched_barrier(0);
       };
-      // ---- per 32-query half: P = exp(S - L), dS = P (dP - D), then
-      //      dV += P^T dO and dK += dS^T Q (A operands straight from registers,
-      //      B operands by transposed reads of the row-major Q / dO tiles), and
-      //      dS^T -> LDS.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of
-      //      the block and key 32w + lc of the tile.  Keys past N need no mask:
-      //      their K, V rows read as zero and their dK, dV rows are not stored.
-      //      The second half's exp work is interleaved with the first half's MFMAs.
-      softmax_grad(0);
-      store_ds(0);
-      softmax_grad(1);
-      store_ds(1);
-      dvdk(0);
-      dvdk(1);
 
-      // deferred release of the previous block: its accumulator stores were
-      // followed by at least 9 vector memory operations (the counter poll and
-      // this block's Q / dO loads), and these complete in issue order, so at
-      // most 8 outstanding means the stores are done
+      // run 1: S/dP of half 0, with the next block's Q / dO / L / D prefetch
+      sdp(0, [&](int ks) {
+        if (pb_next < 0) return;
+        if (ks < QLD) load_part(pb_next, buf ^ 1, ks);
+        if (ks == 0) load_ld(pb_next, buf ^ 1);
+      });
+      // ---- ordering: the counter of this block was loaded at the end of the
+      //      previous step; if the turn is ours, fetch the accumulator slice
+      //      during the next run so its latency hides behind the MFMAs
+      if (ordered && !failed) {
+        const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
+        if (v0 == NW * rank) {
+          have_turn = true;
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        }
+      }
+      const bool early_acc = ordered && have_turn && rank > 0;
+      read_ld(0, 0);
+      // run 2: S/dP of half 1, with softmax of half 0 and the accumulator fetch
+      sdp(1, [&](int ks) {
+#pragma unroll
+        for (int p = ks * 8 / KS; p < (ks + 1) * 8 / KS; ++p) {
+          softmax_piece(0, p);
+          if (early_acc) lds_load16_coherent(racc, &acc_w[p * 256], acc_off(pb, p));
+        }
+      });
+      // run 3: dV/dK of half 0, with softmax of half 1
+      dvdk(0, [&](int k) {
+#pragma unroll
+        for (int p = k * 8 / (2 * NB); p < (k + 1) * 8 / (2 * NB); ++p) softmax_piece(1, p);
+      });
+      // run 4: dV/dK of half 1, with the dS^T stores
+      dvdk(1, [&](int k) {
+#pragma unroll
+        for (int p = k * 8 / (2 * NB); p < (k + 1) * 8 / (2 * NB); ++p) store_ds_piece(p);
+      });
+
+      // deferred release of the previous block: when this step prefetched,
+      // its accumulator stores were followed by the 2*QLD = 8 Q / dO loads of
+      // the prefetch (and possibly more), and vector memory operations complete
+      // in issue order, so at most 8 outstanding means the stores are done;
+      // without a prefetch, wait for everything
       if (pend_ctr >= 0) {
-        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        if (pb_next >= 0)
+          asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+        else
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         release();
       }
       __syncthreads();
@@ -546,6 +573,9 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       }
       // this wave's slice (and the next block's Q / dO) have landed
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // sample the next block's counter now, ahead of the stores below
+      if (ordered && pb_next >= 0)
+        poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if constexpr (ordered) {
         // ---- add this wave's partial into its slice straight from registers:
         //      the accumulator is stored in this wave's register order, so the
@@ -600,8 +630,6 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           release();
         }
       }
-      if (ordered && pb_next >= 0)
-        poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       buf ^= 1;
       st = nst;
     }
