@@ -97,6 +97,12 @@ typedef struct {
      a caller can time that kernel alone. */
   void* event_main_begin;
   void* event_main_end;
+  /* If > 0: at most this many persistent workgroups for the main kernel (0 =
+     as many as the GPU keeps resident).  Must be at least the number of KV-tile
+     chains of one head (T_c, or T_c/2 for Symmetric Shift), else
+     DASH_ERR_INVALID_ARG.  The summation order -- hence every output bit --
+     does not depend on it. */
+  int max_workgroups;
 } dash_bwd_options_t;
 
 /*

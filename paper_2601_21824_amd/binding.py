@@ -39,7 +39,7 @@ class dash_bwd_options_t(ctypes.Structure):
     _fields_ = [("spin_limit", ctypes.c_int), ("flags", ctypes.c_int),
                 ("witness", ctypes.c_void_p), ("partials", ctypes.c_void_p),
                 ("dq_accum", ctypes.c_void_p), ("event_main_begin", ctypes.c_void_p),
-                ("event_main_end", ctypes.c_void_p)]
+                ("event_main_end", ctypes.c_void_p), ("max_workgroups", ctypes.c_int)]
 
 
 _lib = None

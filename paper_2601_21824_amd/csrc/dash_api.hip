@@ -174,6 +174,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
     return fail(DASH_ERR_INVALID_ARG, "workspace missing or smaller than dash_bwd_workspace_size()");
   if (((uintptr_t)workspace & 255) != 0) return fail(DASH_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (opts && opts->spin_limit < 0) return fail(DASH_ERR_INVALID_ARG, "spin_limit must be >= 0");
+  if (opts && opts->max_workgroups < 0) return fail(DASH_ERR_INVALID_ARG, "max_workgroups must be >= 0");
   DeviceInfo di;
   if ((rc = device_info(&di))) return rc;
 
@@ -188,7 +189,13 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   if ((long)(G.t_r + 1) * G.nsub > dash::kMaxChainSteps || N > 32768)
     return fail(DASH_ERR_UNSUPPORTED, "sequence too long for one workgroup chain (N <= 32768)");
   const long items = (long)B * H * G.chains;
-  const int grid = (int)(items < resident ? items : resident);
+  long cap = resident;
+  if (opts && opts->max_workgroups > 0) {
+    if (sched != DASH_SCHED_ATOMIC && opts->max_workgroups < G.chains)
+      return fail(DASH_ERR_INVALID_ARG, "max_workgroups is below the KV-tile chains of one head");
+    if (opts->max_workgroups < cap) cap = opts->max_workgroups;
+  }
+  const int grid = (int)(items < cap ? items : cap);
 
   char* ws = (char*)workspace;
   dash::BwdArgs a;

@@ -101,6 +101,40 @@ def test_witness_and_partial_sum_replay(case):
     assert torch.equal(want_dq.view(torch.int16), dq.cpu().reshape(B * H, N, d).view(torch.int16))
 
 
+GRID_CASES = [
+    (2, 4, 2048, 128, False, "shift"),
+    (2, 4, 2048, 128, False, "naive"),
+    (2, 4, 2048, 128, True, "symshift"),
+    (2, 4, 2048, 128, True, "descending"),
+    (2, 8, 1024, 64, True, "symshift"),
+]
+
+
+@pytest.mark.parametrize("case", GRID_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in GRID_CASES])
+def test_grid_size_does_not_change_bits(case):
+    """The summation order is a function of the schedule and shape only: the
+    persistent grid's size (from one head's chains up to the GPU's resident
+    count) leaves every output bit unchanged; below one head's chains the call
+    is rejected."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[grid] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=31)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    chains = dash.dash_schedule_table(sched, N, d, causal)["chains"]
+    ws = dash.new_workspace(B, H, N, d)
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
+    for cap in (chains, chains + 3, 2 * chains + 1):
+        opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap)
+        got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts, workspace=ws)
+        assert dash.dash_bwd_check(ws) == dash.DASH_OK
+        for a, b in zip(ref, got):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"grid {cap} differs"
+    with pytest.raises(dash.DashError) as e:
+        run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws,
+                options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, chains - 1))
+    assert e.value.code == dash.DASH_ERR_INVALID_ARG
+
+
 def test_watchdog_reports_timeout_and_library_recovers():
     """Counters poisoned from the host: every first wait times out after a few
     polls, the kernels still exit, the call reports DASH_ERR_TIMEOUT, and the
