@@ -14,7 +14,7 @@
  *    each query row (the "logsumexp vector L" that Algorithm 1 takes as input).
  *  - Self-attention only: N queries attend to N keys.  With causal != 0,
  *    query i sees key j iff j <= i.
- *  - d must be 64 or 128.  N >= 0 is arbitrary (ragged last tiles are masked);
+ *  - d must be 64, 128 or 256.  N >= 0 is arbitrary (ragged last tiles are masked);
  *    B, H >= 0.  A problem with B*H*N == 0 is a successful no-op.
  *  - scale is the softmax scale s in S = s * Q K^T (the _ex forms take it;
  *    the others use 1/sqrt(d)).  dQ and dK include the factor s, dV does not.
@@ -61,7 +61,7 @@ typedef enum {
 
 typedef enum {
   DASH_OK = 0,
-  DASH_ERR_INVALID_ARG = -1, /* null pointer, negative size, d not 64/128, bad enum */
+  DASH_ERR_INVALID_ARG = -1, /* null pointer, negative size, d not 64/128/256, bad enum */
   DASH_ERR_UNSUPPORTED = -2, /* valid request this build cannot run (e.g. SYMSHIFT
                                 with a full mask, too many KV tiles per head) */
   DASH_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
@@ -82,12 +82,14 @@ typedef struct {
   int spin_limit;
   /* DASH_FLAG_* bits */
   int flags;
-  /* If non-NULL: int32 [B*H][ceil(N/64)][T_c], T_c = ceil(N/d) KV tiles.  The
-     workgroup that adds its partial to 64-row dQ block p with order position r
-     writes its KV-tile index at [bh][p][r] (ordering witness). */
+  /* If non-NULL: int32 [B*H][ceil(N/64)][T_c], T_c = ceil(N/bc) KV tiles of
+     bc rows (bc = d for d <= 128, 64 for d = 256; geometry[4] of
+     dash_schedule_table).  The workgroup that adds its partial to 64-row dQ
+     block p with order position r writes its KV-tile index at [bh][p][r]
+     (ordering witness). */
   int32_t* witness;
-  /* If non-NULL: fp32 [B*H][T_c][N][d].  Each KV tile's unscaled dQ partial
-     (its dS K for every query row) is written at [bh][j]. */
+  /* If non-NULL: fp32 [B*H][T_c][N][d], T_c as above.  Each KV tile's
+     unscaled dQ partial (its dS K for every query row) is written at [bh][j]. */
   float* partials;
   /* If non-NULL: fp32 [B*H][N][d].  Receives the final unscaled fp32 dQ sum
      (deterministic schedules only). */
@@ -98,10 +100,11 @@ typedef struct {
   void* event_main_begin;
   void* event_main_end;
   /* If > 0: at most this many persistent workgroups for the main kernel (0 =
-     as many as the GPU keeps resident).  Must be at least the number of KV-tile
-     chains of one head (T_c, or T_c/2 for Symmetric Shift), else
-     DASH_ERR_INVALID_ARG.  The summation order -- hence every output bit --
-     does not depend on it. */
+     as many as the GPU keeps resident).  Shift needs at least the chains of
+     one group (geometry[5] of dash_schedule_table), Symmetric Shift the
+     chains of one head, else DASH_ERR_INVALID_ARG; naive, Descending and
+     atomic run with any count.  The summation order -- hence every output
+     bit -- does not depend on it. */
   int max_workgroups;
 } dash_bwd_options_t;
 
@@ -156,8 +159,12 @@ int dash_resolve_schedule(int schedule, int d, int causal);
 /*
  * Host-side view of the schedule the kernels follow (no GPU needed).  For one
  * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c
- * KV tiles of bc = d rows.  Writes, when the pointer is non-NULL:
- *   geometry[4]            = {T_r, T_c, br, number of workgroups per head}
+ * KV tiles of bc rows (bc = d for d <= 128, 64 for d = 256).  Writes, when the
+ * pointer is non-NULL:
+ *   geometry[6]            = {T_r, T_c, br, number of workgroup chains per
+ *                             head, bc, chains per Shift group (the chains
+ *                             that must run at the same time; = chains for
+ *                             the other schedules)}
  *   chain_len[w]           = tasks of workgroup w
  *   task_kv[w*cap + t], task_q[w*cap + t] = the t-th task of workgroup w,
  *                            cap = max chain length = geometry-dependent

@@ -19,7 +19,11 @@ the accumulation order is *derived* by sorting rather than by a formula:
   Full Masks"): workgroup j starts at a cyclically shifted Q tile; the dQ
   order follows the visiting timestamps (Fig. 6 caption: distinct timestamps
   per dQ row induce the reduction sequence).  With T_r = g*T_c Q tiles the
-  shift is g tiles per workgroup (reading for unequal tile sizes).
+  shift is g tiles per workgroup (reading for unequal tile sizes).  When the
+  workgroups of one head cannot all run at once (the "refine or aggregate
+  heads" case of Section 3.1), the KV tiles are cut into groups of `group`
+  consecutive tiles: each dQ tile sums group 0's partials in visiting order,
+  then group 1's, and so on.
 * SYMSHIFT -- Symmetric Shift, causal mask (Section 3.4, "Symmetric Shift
   Scheduling for Causal Masks"): workgroup p owns KV tiles p and T-1-p; phase 1
   is a cyclic shift over the dense lower-left rectangle, phase 2 walks the
@@ -67,8 +71,9 @@ class Schedule:
         return out
 
 
-def build(kind: str, t_r: int, t_c: int, causal: bool, br: int, bc: int) -> Schedule:
-    """Enumerate one head's schedule for t_r Q tiles and t_c KV tiles."""
+def build(kind: str, t_r: int, t_c: int, causal: bool, br: int, bc: int, group: int | None = None) -> Schedule:
+    """Enumerate one head's schedule for t_r Q tiles and t_c KV tiles
+    (`group`: SHIFT only, KV tiles per group; None = one group)."""
     valid_q = {j: [i for i in range(t_r) if interacts(i, j, br, bc, causal)] for j in range(t_c)}
     if kind == NAIVE:
         chains = [[(j, i) for i in valid_q[j]] for j in range(t_c)]
@@ -110,13 +115,15 @@ def build(kind: str, t_r: int, t_c: int, causal: bool, br: int, bc: int) -> Sche
         for t, (j, i) in enumerate(ch):
             contributors[i].append((t, j))
     if by_timestamp:
-        order = {i: [j for (t, j) in sorted(c)] for i, c in contributors.items()}
+        gsize = group if (kind == SHIFT and group) else t_c
+        order = {i: [j for (_, t, j) in sorted((j // gsize, t, j) for (t, j) in c)]
+                 for i, c in contributors.items()}
     else:
         order = {i: sorted(j for (t, j) in c) for i, c in contributors.items()}
     return Schedule(chains, order)
 
 
-def check(s: Schedule, t_r: int, t_c: int, causal: bool, br: int, bc: int) -> dict:
+def check(s: Schedule, t_r: int, t_c: int, causal: bool, br: int, bc: int, group: int | None = None) -> dict:
     """Structural properties the paper asks of a schedule.
 
     coverage     -- every interacting (Q tile, KV tile) pair runs exactly once
@@ -127,7 +134,9 @@ def check(s: Schedule, t_r: int, t_c: int, causal: bool, br: int, bc: int) -> di
     monotone     -- along each dQ tile's accumulation order the step strictly
                     increases, i.e. every ordering edge goes from the end of a
                     reduction to the start of a deeper one (Lemma 1's condition
-                    depth(u) <= depth(v) on the chain DAG)
+                    depth(u) <= depth(v) on the chain DAG); with groups, within
+                    each group's part of the order (later groups run after
+                    earlier ones, so no edge between groups can close a cycle)
     """
     pairs = [(i, j) for ch in s.chains for (j, i) in ch]
     want = {(i, j) for i in range(t_r) for j in range(t_c) if interacts(i, j, br, bc, causal)}
@@ -149,10 +158,12 @@ def check(s: Schedule, t_r: int, t_c: int, causal: bool, br: int, bc: int) -> di
         per_step.setdefault(t, []).append(i)
     conflict_free = all(len(v) == len(set(v)) for v in per_step.values())
     monotone = True
+    gsize = group or t_c
     for i, js in s.order.items():
-        ts = [step[(i, j)][1] for j in js]
-        if any(b <= a for a, b in zip(ts, ts[1:])):
-            monotone = False
+        for g0 in range(0, t_c, gsize):
+            ts = [step[(i, j)][1] for j in js if g0 <= j < g0 + gsize]
+            if any(b <= a for a, b in zip(ts, ts[1:])):
+                monotone = False
     return dict(coverage=coverage, contiguous=contiguous, conflict_free=conflict_free,
                 monotone=monotone)
 

@@ -168,9 +168,9 @@ def dash_bwd_check(workspace, stream=None) -> int:
 def dash_schedule_table(schedule, N: int, d: int, causal: bool) -> dict:
     """The schedule the kernels follow for one head (host computation)."""
     lib = load()
-    geo = (ctypes.c_int * 4)()
+    geo = (ctypes.c_int * 6)()
     _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), geo, None, None, None, None))
-    t_r, t_c, br, chains = list(geo)
+    t_r, t_c, br, chains, bc, grp = list(geo)
     cap = t_r + 1
     chain_len = np.zeros(chains, np.int32)
     task_kv = np.full(chains * cap, -1, np.int32)
@@ -179,7 +179,7 @@ def dash_schedule_table(schedule, N: int, d: int, causal: bool) -> dict:
     p = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
     _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), geo, p(chain_len), p(task_kv),
                                    p(task_q), p(rank)))
-    return dict(t_r=t_r, t_c=t_c, br=br, chains=chains, chain_len=chain_len,
+    return dict(t_r=t_r, t_c=t_c, br=br, chains=chains, bc=bc, group=grp, chain_len=chain_len,
                 task_kv=task_kv.reshape(chains, cap), task_q=task_q.reshape(chains, cap),
                 rank=rank.reshape(t_r, t_c))
 

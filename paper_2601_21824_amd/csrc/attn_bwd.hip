@@ -22,6 +22,7 @@
 // bwd_post : atomic variant only: dQ = bf16(s * dQacc).
 #include "common.h"
 #include "kernels.h"
+#include "bwd_common.h"
 
 namespace dash {
 
@@ -84,22 +85,6 @@ __global__ __launch_bounds__(256) void bwd_post_kernel(BwdArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- ordering
-// Spin until *ctr == want (relaxed, device-coherent loads).  Wave-uniform.
-// A block's counter advances by one per wave of each contributor, so rank r
-// holds the turn when it reads (waves per workgroup) * r.
-// Returns false after `limit` polls; the caller then skips its update.
-__device__ inline bool wait_turn(const int* ctr, int want, int limit) {
-  for (int n = 0;; ++n) {
-    const int v = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    if (v == want) break;
-    if (n >= limit) return false;
-    __builtin_amdgcn_s_sleep(2);
-  }
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the data loads after the wait
-  return true;
-}
-
 // ---------------------------------------------------------------- bwd_main
 // LDS tiles of bf16 rows are stored in 16-byte chunks with chunk c of row r at
 // c ^ sw16(r): 8 consecutive rows read at the same chunk (MFMA row operands)
@@ -121,50 +106,6 @@ __device__ inline int f_at(int r, int col) {  // element index in a [rows][D] fp
 // bank-conflict free.
 __device__ inline int swt(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
 __device__ inline int dst_at(int r, int q) { return r * kBlockRows + (((q >> 2) ^ swt(r)) << 2); }
-
-// 4 bf16 of one column from 4 consecutive rows (gfx950 transpose read): within
-// each group of 16 lanes, lane L addresses row L/4, columns 4*(L%4)..+3 of a
-// 4 x 16 tile and receives column L of it.
-__device__ inline u32x2 tr_read(const __bf16* p) {
-  typedef short s16x4 __attribute__((__vector_size__(8)));
-  s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
-  return __builtin_bit_cast(u32x2, v);
-}
-
-// Direct global -> LDS load of 16 (or 4) bytes per lane: lane i of the wave
-// writes bytes [16i, 16i+16) after the wave-uniform LDS base `dst`.
-typedef __attribute__((address_space(3))) void* lds_ptr;
-__device__ inline void lds_load16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, 0);
-}
-__device__ inline void lds_load16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, kCoherent);
-}
-__device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
-}
-
-// Scheduling hints (one wave per SIMD, so latency must be hidden inside the
-// wave): keep `AHEAD` LDS reads in flight ahead of a run of N MFMAs, then
-// issue PER reads and VALU_PER vector ops after each MFMA.
-template <int N, int AHEAD, int PER, int VALU_PER>
-__device__ inline void sched_mfma_pipeline() {
-  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD, 0);
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    if (PER) __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);
-    if (VALU_PER) __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0);
-  }
-}
-
-// One step of a chain, packed for the LDS step table: 64-row block pb (12
-// bits), KV tile j (9), rank in the block's summation order (10), last (1).
-// kNoStep marks a step whose block or KV tile lies past N.
-constexpr unsigned kNoStep = 0xffffffffu;
-__device__ inline unsigned pack_step(int pb, int j, int rank, bool last) {
-  return (unsigned)pb | ((unsigned)j << 12) | ((unsigned)rank << 21) | ((unsigned)last << 31);
-}
 
 template <int D>
 struct MainSmem {
@@ -656,7 +597,10 @@ void launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t st
   const bool atomic = a.G.sched == S_ATOMIC;
   hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
-  launch_main<D>(a, grid_main, stream);
+  if constexpr (D == 256)
+    launch_main256(a, grid_main, stream);
+  else
+    launch_main<D>(a, grid_main, stream);
   if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
   if (atomic) hipLaunchKernelGGL(bwd_post_kernel<D>, dim3(1024), dim3(256), 0, stream, a);
 }
@@ -669,8 +613,10 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
   if (pre_blocks > 65535L * 16) pre_blocks = 65535L * 16;
   if (d == 64)
     launch_all<64>(a, pre_blocks, grid_main, stream);
-  else
+  else if (d == 128)
     launch_all<128>(a, pre_blocks, grid_main, stream);
+  else
+    launch_all<256>(a, pre_blocks, grid_main, stream);
   return hipGetLastError();
 }
 
@@ -687,6 +633,8 @@ int main_occupancy() {
   return lo;
 }
 
-int bwd_main_occupancy(int d) { return d == 64 ? main_occupancy<64>() : main_occupancy<128>(); }
+int bwd_main_occupancy(int d) {
+  return d == 64 ? main_occupancy<64>() : d == 128 ? main_occupancy<128>() : bwd_main256_occupancy();
+}
 
 }  // namespace dash

@@ -45,14 +45,14 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
   float m = -INFINITY, lsum = 0.f;
 
   const int kv_end = a.causal ? min(N, q0 + 128) : N;
-  // loader unit: 4 rows x 8 columns
+  // loader unit: 4 rows x 8 columns; 16 * CPR units per KV block
   constexpr int CPR = D / 8;
-  const int lu_c = tid % CPR, lu_rg = tid / CPR;
-  const bool loader = tid < 16 * CPR;
 
   for (int kv0 = 0; kv0 < kv_end; kv0 += KB) {
     __syncthreads();
-    if (loader) {
+#pragma unroll
+    for (int unit = tid; unit < 16 * CPR; unit += 256) {
+      const int lu_c = unit % CPR, lu_rg = unit / CPR;
       u32x4 kr[4], vr[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -153,8 +153,10 @@ hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream) {
   dim3 grid((a.n + 127) / 128, a.bh);
   if (d == 64)
     hipLaunchKernelGGL(attn_fwd_kernel<64>, grid, dim3(256), 0, stream, a);
-  else
+  else if (d == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_fwd_kernel<256>, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -54,7 +54,7 @@ Layout layout(int B, int H, int N, int d) {
 struct DeviceInfo {
   int device = -1;
   int cus = 0;
-  int occ64 = 0, occ128 = 0;
+  int occ64 = 0, occ128 = 0, occ256 = 0;
 };
 
 std::mutex g_mu;
@@ -76,7 +76,8 @@ int device_info(DeviceInfo* out) {
     di.cus = prop.multiProcessorCount;
     di.occ64 = dash::bwd_main_occupancy(64);
     di.occ128 = dash::bwd_main_occupancy(128);
-    if (di.occ64 <= 0 || di.occ128 <= 0) return fail(DASH_ERR_HIP, "occupancy query failed");
+    di.occ256 = dash::bwd_main_occupancy(256);
+    if (di.occ64 <= 0 || di.occ128 <= 0 || di.occ256 <= 0) return fail(DASH_ERR_HIP, "occupancy query failed");
     di.device = dev;
   }
   *out = di;
@@ -85,7 +86,7 @@ int device_info(DeviceInfo* out) {
 
 int check_shape(int B, int H, int N, int d) {
   if (B < 0 || H < 0 || N < 0) return fail(DASH_ERR_INVALID_ARG, "B, H and N must be >= 0");
-  if (d != 64 && d != 128) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  if (d != 64 && d != 128 && d != 256) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64, 128 or 256");
   if ((double)N * d * 4 >= 2147483648.0) return fail(DASH_ERR_INVALID_ARG, "N*d too large (per-head fp32 > 2 GiB)");
   if ((double)B * H >= 2147483647.0 / 1024) return fail(DASH_ERR_INVALID_ARG, "B*H too large");
   return DASH_OK;
@@ -180,19 +181,22 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
 
   const int sched = resolve(schedule, d, causal);
   const dash::Geom G = dash::make_geom(sched, causal, N, d);
-  const int occ = d == 64 ? di.occ64 : di.occ128;
+  const int occ = d == 64 ? di.occ64 : d == 128 ? di.occ128 : di.occ256;
   const long resident = (long)occ * di.cus;
-  // Every chain of one head must be able to run at once: a chain may wait on
-  // any other chain of its head (persistent grid, in-order work tickets).
-  if (sched != DASH_SCHED_ATOMIC && G.chains > resident)
+  // Shift-type chains wait on each other in a cycle: every chain of a Shift
+  // group (Symmetric Shift: of a head) must be able to run at once.  Naive and
+  // Descending chains only wait on chains with lower work tickets, which the
+  // in-order ticket counter has already started, so any grid size works.
+  const long coresident = sched == DASH_SCHED_SHIFT ? G.grp : sched == DASH_SCHED_SYMSHIFT ? G.chains : 1;
+  if (coresident > resident)
     return fail(DASH_ERR_UNSUPPORTED, "too many KV tiles per head for the resident workgroups of this GPU");
   if ((long)(G.t_r + 1) * G.nsub > dash::kMaxChainSteps || N > 32768)
     return fail(DASH_ERR_UNSUPPORTED, "sequence too long for one workgroup chain (N <= 32768)");
   const long items = (long)B * H * G.chains;
   long cap = resident;
   if (opts && opts->max_workgroups > 0) {
-    if (sched != DASH_SCHED_ATOMIC && opts->max_workgroups < G.chains)
-      return fail(DASH_ERR_INVALID_ARG, "max_workgroups is below the KV-tile chains of one head");
+    if (opts->max_workgroups < coresident)
+      return fail(DASH_ERR_INVALID_ARG, "max_workgroups is below the chains that must run at once");
     if (opts->max_workgroups < cap) cap = opts->max_workgroups;
   }
   const int grid = (int)(items < cap ? items : cap);
@@ -219,7 +223,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   a.bh = B * H;
   a.n = N;
   a.nblk = (N + dash::kBlockRows - 1) / dash::kBlockRows;
-  a.tc = (N + d - 1) / d;
+  a.tc = (N + G.bc - 1) / G.bc;  // real KV tiles (before Symmetric Shift's padding)
   a.scale = scale;
   a.spin_limit = (opts && opts->spin_limit > 0) ? opts->spin_limit : (1 << 24);
   a.poison = (opts && (opts->flags & DASH_FLAG_POISON_COUNTERS)) ? 1 : 0;
@@ -245,7 +249,7 @@ int dash_bwd_check(void* workspace, void* stream) {
 
 int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
                   void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule) {
-  if (d != 64 && d != 128) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  if (d != 64 && d != 128 && d != 256) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64, 128 or 256");
   const float scale = 1.0f / std::sqrt((float)d);
   int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
   if (rc) return rc;
@@ -285,6 +289,8 @@ int dash_schedule_table(int schedule, int N, int d, int causal, int* geometry, i
     geometry[1] = G.t_c;
     geometry[2] = G.br;
     geometry[3] = G.chains;
+    geometry[4] = G.bc;
+    geometry[5] = G.grp;
   }
   const int cap = G.t_r + 1;
   for (int w = 0; w < G.chains; ++w) {

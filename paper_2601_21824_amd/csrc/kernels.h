@@ -53,5 +53,8 @@ struct BwdArgs {
 hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream);
 int bwd_main_occupancy(int d);
+// head dim 256 (attn_bwd256.hip)
+void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream);
+int bwd_main256_occupancy();
 
 }  // namespace dash

@@ -1,7 +1,8 @@
 // schedule.h -- closed-form dQ-reduction schedules, usable on host and device.
 //
-// One attention head of N rows is cut into KV tiles of BC = d rows (one
-// workgroup's resident K_j, V_j, dK_j, dV_j) and scheduling Q tiles of br rows;
+// One attention head of N rows is cut into KV tiles of BC rows (BC = d for
+// d <= 128, 64 for d = 256: one workgroup's resident K_j, V_j, dK_j, dV_j)
+// and scheduling Q tiles of br rows;
 // a scheduling Q tile is processed as br/64 physical 64-row blocks, each with
 // its own ordering counter.  A workgroup runs a "chain" of tasks (KV tile j,
 // Q tile i); the dQ partials of Q tile i are added in the order rank(i, j).
@@ -12,7 +13,10 @@
 //                 to first, summation order unchanged (ascending KV).
 //  SHIFT       -- Shift Scheduling (Section 3.4, full mask): workgroup j visits
 //                 Q tiles (j*g + t) mod T_r, g = T_r / T_c; the summation order is
-//                 the visiting order, so rank = (i/g - j) mod T_c.
+//                 the visiting order, so rank = (i/g - j) mod T_c.  A head with
+//                 more than kMaxGroup KV tiles is split into groups of kMaxGroup
+//                 consecutive tiles whose chains must run at the same time; the
+//                 order is group-major and the visiting order within a group.
 //  SYMSHIFT    -- Symmetric Shift (Section 3.4, causal): workgroup p owns KV tiles
 //                 p and T-1-p (T even, h = T/2).  Phase 1 (steps 0..h-1): Q tile
 //                 h + (p+t) mod h with KV p (dense lower-left rectangle).  Phase 2
@@ -38,6 +42,7 @@ namespace dash {
 enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4 };
 
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
+constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident
 
 struct Geom {
   int sched;   // Sched
@@ -49,20 +54,25 @@ struct Geom {
   int t_r;     // scheduling Q tiles per head (= g * t_c)
   int nsub;    // physical 64-row blocks per scheduling Q tile (= br / 64)
   int chains;  // workgroup chains per head
+  int grp;     // SHIFT: chains per group (others: = chains)
 };
+
+// rows per KV tile for head dim d
+DASH_HD int kv_tile_rows(int d) { return d <= 128 ? d : 64; }
 
 DASH_HD Geom make_geom(int sched, int causal, int N, int d) {
   Geom G;
   G.sched = sched;
   G.causal = causal ? 1 : 0;
-  G.bc = d;
-  G.br = causal ? d : kBlockRows;
+  G.bc = kv_tile_rows(d);
+  G.br = causal ? G.bc : kBlockRows;
   G.g = G.bc / G.br;
   G.t_c = (N + G.bc - 1) / G.bc;
   if (sched == S_SYMSHIFT) G.t_c += G.t_c & 1;
   G.t_r = G.g * G.t_c;
   G.nsub = G.br / kBlockRows;
   G.chains = sched == S_SYMSHIFT ? G.t_c / 2 : G.t_c;
+  G.grp = (sched == S_SHIFT && G.chains > kMaxGroup) ? kMaxGroup : G.chains;
   return G;
 }
 
@@ -126,8 +136,17 @@ DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
 // position of KV tile j in Q tile i's summation order
 DASH_HD int rank_of(const Geom& G, int i, int j) {
   switch (G.sched) {
-    case S_SHIFT:
-      return pmod(i / G.g - j, G.t_c);
+    case S_SHIFT: {
+      // group-major; inside a group (tiles j0 .. j0+s-1) the visiting order:
+      // with a = i/g and u = (a - j0) mod T_c, tile j0+v visits Q tile i at
+      // step ((a - j0 - v) mod T_c) * g + i % g, so it comes after the tiles
+      // v' in (v, min(u, s-1)] when v <= u, else after all v' <= u and v' > v
+      const int j0 = j - j % G.grp;
+      const int sz = G.t_c - j0 < G.grp ? G.t_c - j0 : G.grp;
+      const int v = j - j0, u = pmod(i / G.g - j0, G.t_c);
+      const int top = u < sz - 1 ? u : sz - 1;
+      return j0 + (v <= u ? top - v : u + sz - v);
+    }
     case S_SYMSHIFT: {
       const int h = G.t_r / 2;
       if (i < h) return i - j;

@@ -71,8 +71,8 @@ KINDS = {b.DASH_SCHED_NAIVE: osched.NAIVE, b.DASH_SCHED_DESCENDING: osched.DESCE
          b.DASH_SCHED_ATOMIC: osched.NAIVE}
 
 
-@pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 8192, 16384])
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 8192, 16384, 32768])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("sched", [0, 1, 2, 3, 4])
 def test_schedule_table_matches_oracle(sched, causal, N, d):
@@ -81,10 +81,13 @@ def test_schedule_table_matches_oracle(sched, causal, N, d):
     tab = b.dash_schedule_table(sched, N, d, causal)
     concrete = b.dash_resolve_schedule(sched, d, causal)
     kind = KINDS[concrete]
-    t_r, t_c, br = tab["t_r"], tab["t_c"], tab["br"]
-    # tile sizes: KV tiles of d rows; Q tiles of 64 rows (full) or d rows (causal)
-    assert br == (d if causal else 64) and t_r * br == t_c * d
-    ref = osched.build(kind, t_r, t_c, causal, br, d)
+    t_r, t_c, br, bc, grp = tab["t_r"], tab["t_c"], tab["br"], tab["bc"], tab["group"]
+    # tile sizes: KV tiles of d rows (64 at d = 256); Q tiles of 64 rows (full)
+    # or KV-tile rows (causal); Shift groups of at most 256 chains
+    assert bc == (d if d <= 128 else 64)
+    assert br == (bc if causal else 64) and t_r * br == t_c * bc
+    assert grp == (min(t_c, 256) if kind == osched.SHIFT else tab["chains"])
+    ref = osched.build(kind, t_r, t_c, causal, br, bc, group=grp if kind == osched.SHIFT else None)
     assert tab["chains"] == len(ref.chains)
     for w, ch in enumerate(ref.chains):
         n = tab["chain_len"][w]
@@ -97,5 +100,5 @@ def test_schedule_table_matches_oracle(sched, causal, N, d):
             want[i, j] = r
     np.testing.assert_array_equal(tab["rank"], want)
     if kind in (osched.SHIFT, osched.SYMSHIFT):
-        props = osched.check(ref, t_r, t_c, causal, br, d)
-        assert props["conflict_free"] and props["monotone"]
+        props = osched.check(ref, t_r, t_c, causal, br, bc, group=grp if kind == osched.SHIFT else None)
+        assert props["coverage"] and props["conflict_free"] and props["monotone"]

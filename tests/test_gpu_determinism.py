@@ -22,6 +22,8 @@ DET_CASES = [
     (2, 4, 2048, 128, False, "naive"),
     (2, 4, 2048, 128, True, "descending"),
     (2, 4, 2048, 128, True, "symshift"),
+    (1, 2, 1024, 256, False, "shift"),
+    (1, 2, 1024, 256, True, "symshift"),
 ]
 
 
@@ -61,6 +63,9 @@ PROTO_CASES = [
     (1, 2, 512, 128, True, "descending"),
     (2, 1, 300, 64, True, "symshift"),
     (2, 1, 300, 128, False, "shift"),
+    (1, 2, 512, 256, False, "shift"),
+    (1, 2, 512, 256, True, "symshift"),
+    (1, 1, 333, 256, True, "descending"),
 ]
 
 
@@ -74,7 +79,8 @@ def test_witness_and_partial_sum_replay(case):
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=21)
     og, lseg = run_fwd(qg, kg, vg, causal)
     nblk = (N + 63) // 64
-    tc = (N + d - 1) // d
+    tab = dash.dash_schedule_table(sched, N, d, causal)
+    tc = (N + tab["bc"] - 1) // tab["bc"]  # KV tiles (before Symmetric Shift's padding)
     witness = torch.full((B * H, nblk, tc), -1, dtype=torch.int32, device="cuda")
     partials = torch.full((B * H, tc, N, d), float("nan"), dtype=torch.float32, device="cuda")
     acc = torch.full((B * H, N, d), float("nan"), dtype=torch.float32, device="cuda")
@@ -83,7 +89,8 @@ def test_witness_and_partial_sum_replay(case):
     tab = dash.dash_schedule_table(sched, N, d, causal)
     kind = {"shift": osched.SHIFT, "naive": osched.NAIVE, "descending": osched.DESCENDING,
             "symshift": osched.SYMSHIFT}[sched]
-    ref = osched.build(kind, tab["t_r"], tab["t_c"], causal, tab["br"], d)
+    ref = osched.build(kind, tab["t_r"], tab["t_c"], causal, tab["br"], tab["bc"],
+                       group=tab["group"] if kind == osched.SHIFT else None)
     nsub = tab["br"] // 64
     W = witness.cpu().numpy()
     P = partials.cpu().numpy()
@@ -120,19 +127,52 @@ def test_grid_size_does_not_change_bits(case):
     print(f"\n[grid] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=31)
     og, lseg = run_fwd(qg, kg, vg, causal)
-    chains = dash.dash_schedule_table(sched, N, d, causal)["chains"]
+    tab = dash.dash_schedule_table(sched, N, d, causal)
+    chains = tab["group"] if sched in ("shift", "symshift") else 1
     ws = dash.new_workspace(B, H, N, d)
     ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
-    for cap in (chains, chains + 3, 2 * chains + 1):
+    for cap in (max(chains, 2), chains + 3, 2 * tab["chains"] + 1):
         opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap)
         got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts, workspace=ws)
         assert dash.dash_bwd_check(ws) == dash.DASH_OK
         for a, b in zip(ref, got):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"grid {cap} differs"
-    with pytest.raises(dash.DashError) as e:
-        run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws,
-                options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, chains - 1))
-    assert e.value.code == dash.DASH_ERR_INVALID_ARG
+    if chains > 1:
+        with pytest.raises(dash.DashError) as e:
+            run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws,
+                    options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, chains - 1))
+        assert e.value.code == dash.DASH_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("d", [64, 256])
+def test_shift_groups_order_and_minimal_grid(d):
+    """N = 32768 gives 512 KV tiles per head at d = 64 and d = 256 (64-row KV
+    tiles), so full-mask Shift runs as two groups of 256 chains: the order the
+    workgroups added their partials in equals the oracle's group-major order,
+    and a grid of exactly one group (256 workgroups) gives the same bits as the
+    default grid."""
+    B, H, N, causal = 1, 1, 32768, False
+    print(f"\n[groups] N={N} d={d}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=41, sigma=0.5)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    tab = dash.dash_schedule_table("shift", N, d, causal)
+    assert tab["t_c"] == 512 and tab["group"] == 256
+    nblk = (N + 63) // 64
+    witness = torch.full((B * H, nblk, tab["t_c"]), -1, dtype=torch.int32, device="cuda")
+    ws = dash.new_workspace(B, H, N, d)
+    opts = dash.dash_bwd_options_t(0, 0, witness.data_ptr(), None, None, None, None, 0)
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, "shift", options=opts, workspace=ws)
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    order = osched.build(osched.SHIFT, tab["t_r"], tab["t_c"], causal, tab["br"], tab["bc"], group=256).order
+    W = witness.cpu().numpy()
+    nsub = tab["br"] // 64
+    for pb in range(nblk):
+        assert W[0, pb].tolist() == order[pb // nsub], pb
+    got = run_bwd(qg, kg, vg, og, dog, lseg, causal, "shift", workspace=ws,
+                  options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 256))
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    for a_, b_ in zip(ref, got):
+        assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
 
 
 def test_watchdog_reports_timeout_and_library_recovers():
