@@ -112,9 +112,10 @@ def sweep(dash, make_inputs, args):
     cases = [(16384 // n, 16, n, 128, False) for n in (512, 1024, 2048, 4096, 8192, 16384)]
     cases += [(16384 // n, 32, n, 128, True) for n in (512, 1024, 2048, 4096, 8192, 16384)]
     cases += [(4, 16, 1024, 64, True)]
+    cases += [(1, 8, 32768, 256, False), (1, 8, 32768, 256, True)]  # long sequence, head dim 256
     for B, H, N, d, causal in cases:
         flops = 4.0 * B * H * N * N * d * 2.5 / (2 if causal else 1)
-        q, k, v, do = make_inputs(B, H, N, d, seed=N + d)
+        q, k, v, do = make_inputs(B, H, N, d, seed=N + d, sigma=0.5 if d == 256 else 1.0)
         qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
         og, lseg = dash.attn_fwd(qg, kg, vg, causal)
         dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
@@ -141,11 +142,14 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--N", type=int, default=8192)
     ap.add_argument("--causal", action="store_true")
+    ap.add_argument("--d", type=int, default=128,
+                    help="head dim; 256 selects the long-sequence workload B=1 H=8 (inputs ~N(0, 0.5^2))")
     ap.add_argument("--schedules", default="",
                     help="comma list of schedules to time (default: the schedule, atomic, naive)")
     ap.add_argument("--sweep", action="store_true",
-                    help="time every schedule over the 16k-token sweeps (full H=16, causal H=32, d=128) and "
-                         "the B=4 H=16 N=1024 d=64 causal case; one JSON line per case")
+                    help="time every schedule over the 16k-token sweeps (full H=16, causal H=32, d=128), "
+                         "the B=4 H=16 N=1024 d=64 causal case and B=1 H=8 N=32768 d=256 (both masks); "
+                         "one JSON line per case")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run 5 plain device copies of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -172,11 +176,13 @@ def main():
     if args.sweep:
         sweep(dash, make_inputs, args)
         return
-    N, d, causal = args.N, 128, args.causal
-    B = max(1, 16384 // N)
-    H = 32 if causal else 16
+    N, d, causal = args.N, args.d, args.causal
+    if d == 256:
+        B, H, sigma = 1, 8, 0.5
+    else:
+        B, H, sigma = max(1, 16384 // N), (32 if causal else 16), 1.0
     flops = 4.0 * B * H * N * N * d * 2.5 / (2 if causal else 1)
-    q, k, v, do = make_inputs(B, H, N, d, seed=1234)
+    q, k, v, do = make_inputs(B, H, N, d, seed=1234, sigma=sigma)
     qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
     og, lseg = dash.attn_fwd(qg, kg, vg, causal)
     dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
@@ -220,10 +226,11 @@ def main():
         "pct_of_atomic": round(100.0 * tflops / results["atomic"][2], 2),
         "atomic_tflops": round(results["atomic"][2], 2),
         "naive_tflops": round(results["naive"][2], 2) if "naive" in results else None,
-        "roofline": {"bound": "mfma", "kernel": "bwd_main_kernel<128, full mask, ordered>",
+        "roofline": {"bound": "mfma", "kernel": f"bwd_main{'256' if d == 256 else ''}_kernel<{d}, "
+                               f"{'causal' if causal else 'full'} mask, {'atomic' if det == 'atomic' else 'ordered'}>",
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic() if (N, causal, det) == (8192, False, "shift") else None,
+                     "traffic": measured_traffic() if (N, d, causal, det) == (8192, 128, False, "shift") else None,
                      "main_kernel_ms": round(main_ms, 4)},
     }
     if not args.no_cpu:

@@ -52,10 +52,11 @@ typedef enum {
   /* Symmetric Shift (Section 3.4, causal masks): KV tiles j and T-1-j share a
      workgroup; two-phase fold.  Causal mask only. */
   DASH_SCHED_SYMSHIFT = 4,
-  /* SHIFT for full masks, SYMSHIFT for causal masks at every head dim.  The
-     paper prefers DESCENDING at d >= 128 because Symmetric Shift costs
-     registers on its hardware (Section 4.3); here its schedule lives in an LDS
-     step table and it is the faster causal schedule at d = 64 and d = 128. */
+  /* SHIFT for full masks.  Causal masks: SYMSHIFT at d = 64 and 128, where it
+     measures faster here (its schedule lives in an LDS step table, so the
+     register cost that makes the paper prefer DESCENDING at d >= 128, Section
+     4.3, does not arise), DESCENDING at d = 256, where it measures faster on
+     long sequences. */
   DASH_SCHED_AUTO = 5
 } dash_schedule_t;
 

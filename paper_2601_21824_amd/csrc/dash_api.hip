@@ -95,7 +95,7 @@ int check_shape(int B, int H, int N, int d) {
 int resolve(int schedule, int d, int causal) {
   switch (schedule) {
     case DASH_SCHED_AUTO:
-      return causal ? DASH_SCHED_SYMSHIFT : DASH_SCHED_SHIFT;
+      return !causal ? DASH_SCHED_SHIFT : (d <= 128 ? DASH_SCHED_SYMSHIFT : DASH_SCHED_DESCENDING);
     case DASH_SCHED_SHIFT:
       return causal ? DASH_SCHED_SYMSHIFT : DASH_SCHED_SHIFT;
     default:
