@@ -186,14 +186,14 @@ def main():
     qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
     og, lseg = dash.attn_fwd(qg, kg, vg, causal)
     dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
-    ws = dash.new_workspace(B, H, N, d)
+    det = args.schedule
+    scheds = [x for x in args.schedules.split(",") if x] or [det, "atomic", "naive"]
+    ws = dash.new_workspace(B, H, N, d, "partials" if "partials" in scheds else det)
     torch.cuda.synchronize()
     tensors = (qg, kg, vg, og, dog, lseg, dq, dk, dv, ws)
     ev = HipEvents()
 
     results = {}
-    det = args.schedule
-    scheds = [x for x in args.schedules.split(",") if x] or [det, "atomic", "naive"]
     for sched in dict.fromkeys(scheds):
         ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
         results[sched] = (ms, main_ms, flops / (ms * 1e-3) / 1e12)

@@ -57,7 +57,13 @@ typedef enum {
      register cost that makes the paper prefer DESCENDING at d >= 128, Section
      4.3, does not arise), DESCENDING at d = 256, where it measures faster on
      long sequences. */
-  DASH_SCHED_AUTO = 5
+  DASH_SCHED_AUTO = 5,
+  /* Comparison point (related work, "Deterministic Implementations"): every
+     KV tile stores its dQ partial in its own fp32 buffer, no ordering waits;
+     a second kernel sums the partials of each dQ tile in ascending KV order.
+     dQ is bitwise equal to NAIVE's; the workspace holds all T_c partials
+     (dash_bwd_workspace_size grows by a factor T_c).  d = 64 and 128. */
+  DASH_SCHED_PARTIALS = 6
 } dash_schedule_t;
 
 typedef enum {
@@ -135,13 +141,14 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
                   const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,
                   int causal, int schedule);
 
-/* Bytes of device workspace dash_attn_bwd_ex needs for this problem (0 if the
-   arguments are invalid).  Independent of the schedule. */
-size_t dash_bwd_workspace_size(int B, int H, int N, int d);
+/* Bytes of device workspace dash_attn_bwd_ex needs for this problem and
+   schedule (0 if the arguments are invalid).  The same for every schedule
+   except DASH_SCHED_PARTIALS, which needs room for all T_c dQ partials. */
+size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule);
 
 /*
  * Asynchronous backward on `stream` with a caller-provided device workspace of
- * ws_bytes >= dash_bwd_workspace_size(B,H,N,d) bytes (256-byte aligned).  The
+ * ws_bytes >= dash_bwd_workspace_size(B,H,N,d,schedule) bytes (256-byte aligned).  The
  * workspace must not be used by another call until this one has finished.
  * A wait timeout is recorded in the workspace; read it with dash_bwd_check.
  */

@@ -17,8 +17,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdash.so")
 
 DASH_SCHED_ATOMIC, DASH_SCHED_NAIVE, DASH_SCHED_DESCENDING = 0, 1, 2
-DASH_SCHED_SHIFT, DASH_SCHED_SYMSHIFT, DASH_SCHED_AUTO = 3, 4, 5
-SCHEDULES = {"atomic": 0, "naive": 1, "descending": 2, "shift": 3, "symshift": 4, "auto": 5}
+DASH_SCHED_SHIFT, DASH_SCHED_SYMSHIFT, DASH_SCHED_AUTO, DASH_SCHED_PARTIALS = 3, 4, 5, 6
+SCHEDULES = {"atomic": 0, "naive": 1, "descending": 2, "shift": 3, "symshift": 4, "auto": 5, "partials": 6}
 DASH_OK, DASH_ERR_INVALID_ARG, DASH_ERR_UNSUPPORTED = 0, -1, -2
 DASH_ERR_HIP, DASH_ERR_TIMEOUT, DASH_ERR_NO_DEVICE = -3, -4, -5
 DASH_FLAG_POISON_COUNTERS = 1
@@ -59,7 +59,7 @@ def load():
         lib.dash_attn_bwd.argtypes = [vp] * 9 + [ci] * 6
         lib.dash_attn_bwd_ex.argtypes = ([vp] * 9 + [ci] * 6 + [cf, vp, sz,
                                          ctypes.POINTER(dash_bwd_options_t), vp])
-        lib.dash_bwd_workspace_size.argtypes = [ci] * 4
+        lib.dash_bwd_workspace_size.argtypes = [ci] * 5
         lib.dash_bwd_workspace_size.restype = sz
         lib.dash_bwd_check.argtypes = [vp, vp]
         lib.dash_resolve_schedule.argtypes = [ci] * 3
@@ -120,8 +120,8 @@ def dash_resolve_schedule(schedule, d: int, causal: bool) -> int:
     return load().dash_resolve_schedule(_sched(schedule), d, int(causal))
 
 
-def dash_bwd_workspace_size(B: int, H: int, N: int, d: int) -> int:
-    return int(load().dash_bwd_workspace_size(B, H, N, d))
+def dash_bwd_workspace_size(B: int, H: int, N: int, d: int, schedule="shift") -> int:
+    return int(load().dash_bwd_workspace_size(B, H, N, d, _sched(schedule)))
 
 
 def dash_attn_fwd(q, k, v, o, lse, causal: bool, scale=None, stream=None):
@@ -185,9 +185,9 @@ def dash_schedule_table(schedule, N: int, d: int, causal: bool) -> dict:
 
 
 # ----------------------------------------------------------------- helpers
-def new_workspace(B, H, N, d):
+def new_workspace(B, H, N, d, schedule="shift"):
     import torch
-    n = dash_bwd_workspace_size(B, H, N, d)
+    n = dash_bwd_workspace_size(B, H, N, d, schedule)
     return torch.empty(max(n, 256), dtype=torch.uint8, device="cuda")
 
 

@@ -85,6 +85,38 @@ __global__ __launch_bounds__(256) void bwd_post_kernel(BwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- bwd_sum_partials
+// PARTIALS variant: dQ = bf16(s * sum_j partial_j), the partials of each
+// 64-row block added in ascending KV order (the order NAIVE's counters
+// enforce, so the result is bitwise NAIVE's).  Partial j of block pb of head
+// bh is the register-order block at ((bh * T_c + j) * nblk + pb) * 64 * D; one
+// thread per 4 floats, consecutive threads on consecutive 16-byte pieces.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_sum_partials_kernel(BwdArgs a) {
+  constexpr int BM = kBlockRows;
+  constexpr int PER = BM * D / 4;  // f32x4 pieces per block
+  const long total = (long)a.bh * a.nblk * PER;
+  const size_t stride_j = (size_t)a.nblk * BM * D;
+  for (long idx = (long)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (long)gridDim.x * 256) {
+    const int e4 = (int)(idx % PER);
+    const long bp = idx / PER;
+    const int pb = (int)(bp % a.nblk), bh = (int)(bp / a.nblk);
+    // register order: slice w (2048 floats), chunk k (256), lane l (4)
+    const int w = e4 >> 9, k = (e4 >> 6) & 7, l = e4 & 63;
+    const int q = pb * BM + 32 * (k >> 2) + (l & 31);
+    const int col = 32 * w + 8 * (k & 3) + 4 * (l >> 5);
+    if (q >= a.n) continue;
+    const int c = contributors(a.G, pb / a.G.nsub);
+    const f32x4* p = (const f32x4*)(a.dqacc + ((size_t)bh * a.tc * a.nblk + pb) * BM * D) + e4;
+    f32x4 s = p[0];
+    for (int j = 1; j < c; ++j) s = s + p[j * stride_j / 4];
+    const float sc = a.scale;
+    u32x2 t = {pack_bf16(s[0] * sc, s[1] * sc), pack_bf16(s[2] * sc, s[3] * sc)};
+    *(u32x2*)((__bf16*)a.dq + ((size_t)bh * a.n + q) * D + col) = t;
+    if (a.dq_accum) *(f32x4*)(a.dq_accum + ((size_t)bh * a.n + q) * D + col) = s;
+  }
+}
+
 // ---------------------------------------------------------------- bwd_main
 // LDS tiles of bf16 rows are stored in 16-byte chunks with chunk c of row r at
 // c ^ sw16(r): 8 consecutive rows read at the same chunk (MFMA row operands)
@@ -120,7 +152,7 @@ struct MainSmem {
   int item;
 };
 
-template <int D, bool CAUSAL, bool ORDERED>
+template <int D, bool CAUSAL, int MODE>
 __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   constexpr int NW = D / 32;    // waves
   constexpr int NT = 64 * NW;   // threads
@@ -145,7 +177,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   const int total = a.bh * G.chains;
-  constexpr bool ordered = ORDERED;  // false: the atomic variant
+  constexpr bool ordered = MODE == kModeOrdered;
   // Shift-type orders are conflict-free: the next contributor to a block reaches
   // it at least one step later, so the counter release can wait until the next
   // step's barrier, by which time the accumulator stores have drained.
@@ -544,6 +576,15 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
             }
           }
         }
+      } else if constexpr (MODE == kModePartials) {
+        // ---- partials variant: the partial goes to KV tile j's own buffer, in
+        //      the same register order as the ordered accumulator
+        const auto rpb = make_rsrc(a.dqacc + ((size_t)bh * a.tc + j) * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int qb = k >> 2, rb = k & 3;
+          st16(rpb, acc_off(pb, k), __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+        }
       } else {
         // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
         //      atomic per element, each instruction covering two whole 128-byte
@@ -579,17 +620,23 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   }
 }
 
+template <int D, bool CAUSAL>
+void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
+  const dim3 grid(grid_main), block(2 * D);
+  if (a.G.sched == S_ATOMIC)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeAtomic>), grid, block, 0, stream, a);
+  else if (a.G.sched == S_PARTIALS)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModePartials>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered>), grid, block, 0, stream, a);
+}
+
 template <int D>
 void launch_main(const BwdArgs& a, int grid_main, hipStream_t stream) {
-  const bool atomic = a.G.sched == S_ATOMIC;
-  const dim3 grid(grid_main), block(2 * D);
-  if (a.G.causal) {
-    if (atomic) hipLaunchKernelGGL((bwd_main_kernel<D, true, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main_kernel<D, true, true>), grid, block, 0, stream, a);
-  } else {
-    if (atomic) hipLaunchKernelGGL((bwd_main_kernel<D, false, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main_kernel<D, false, true>), grid, block, 0, stream, a);
-  }
+  if (a.G.causal)
+    launch_main_mask<D, true>(a, grid_main, stream);
+  else
+    launch_main_mask<D, false>(a, grid_main, stream);
 }
 
 template <int D>
@@ -603,6 +650,8 @@ void launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t st
     launch_main<D>(a, grid_main, stream);
   if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
   if (atomic) hipLaunchKernelGGL(bwd_post_kernel<D>, dim3(1024), dim3(256), 0, stream, a);
+  if constexpr (D <= 128)
+    if (a.G.sched == S_PARTIALS) hipLaunchKernelGGL(bwd_sum_partials_kernel<D>, dim3(4096), dim3(256), 0, stream, a);
 }
 
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream) {
@@ -623,8 +672,9 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 template <int D>
 int main_occupancy() {
   int lo = 1 << 30;
-  const void* fns[4] = {(const void*)bwd_main_kernel<D, false, false>, (const void*)bwd_main_kernel<D, false, true>,
-                        (const void*)bwd_main_kernel<D, true, false>, (const void*)bwd_main_kernel<D, true, true>};
+  const void* fns[6] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
+                        (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeAtomic>,
+                        (const void*)bwd_main_kernel<D, true, kModeOrdered>, (const void*)bwd_main_kernel<D, true, kModePartials>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 2 * D, 0) != hipSuccess) return 0;

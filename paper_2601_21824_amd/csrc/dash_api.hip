@@ -31,16 +31,20 @@ struct Layout {
   size_t ctrl, dqacc, dvec, lse2, counters, total;
 };
 
-// ctrl first so that dash_bwd_check can find it without the problem size
-Layout layout(int B, int H, int N, int d) {
+// ctrl first so that dash_bwd_check can find it without the problem size.
+// `sched` is a resolved schedule: PARTIALS keeps one accumulator-sized buffer
+// per KV tile.
+Layout layout(int B, int H, int N, int d, int sched) {
   Layout L;
   const size_t bh = (size_t)B * H;
   const size_t nblk = ((size_t)N + dash::kBlockRows - 1) / dash::kBlockRows;
+  const size_t bc = dash::kv_tile_rows(d);
+  const size_t copies = sched == DASH_SCHED_PARTIALS ? ((size_t)N + bc - 1) / bc : 1;
   size_t off = 0;
   L.ctrl = off;
   off += dash::kCtrlBytes;
   L.dqacc = off;
-  off += align256(bh * nblk * dash::kBlockRows * d * sizeof(float));  // >= N rows per head
+  off += align256(copies * bh * nblk * dash::kBlockRows * d * sizeof(float));  // >= N rows per head
   L.dvec = off;
   off += align256(bh * N * sizeof(float));
   L.lse2 = off;
@@ -104,7 +108,7 @@ int resolve(int schedule, int d, int causal) {
 }
 
 int check_schedule(int schedule, int causal) {
-  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_AUTO)
+  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_PARTIALS)
     return fail(DASH_ERR_INVALID_ARG, "unknown schedule");
   if (schedule == DASH_SCHED_SYMSHIFT && !causal)
     return fail(DASH_ERR_UNSUPPORTED, "symmetric shift is the causal-mask schedule; use SHIFT for a full mask");
@@ -118,6 +122,8 @@ int check_bwd(const void* q, const void* k, const void* v, const void* o, const 
   int rc = check_shape(B, H, N, d);
   if (rc) return rc;
   if ((rc = check_schedule(schedule, causal))) return rc;
+  if (schedule == DASH_SCHED_PARTIALS && d > 128)
+    return fail(DASH_ERR_UNSUPPORTED, "the partials comparison variant is built for d = 64 and 128");
   if ((size_t)B * H * N == 0) return DASH_OK;
   if (!q || !k || !v || !o || !dO || !lse || !dq || !dk || !dv)
     return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
@@ -137,9 +143,10 @@ const char* dash_last_error(void) { return g_err.c_str(); }
 
 int dash_resolve_schedule(int schedule, int d, int causal) { return resolve(schedule, d, causal); }
 
-size_t dash_bwd_workspace_size(int B, int H, int N, int d) {
+size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule) {
   if (check_shape(B, H, N, d) != DASH_OK) return 0;
-  return layout(B, H, N, d).total;
+  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_PARTIALS) return 0;
+  return layout(B, H, N, d, resolve(schedule, d, 0)).total;
 }
 
 int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N,
@@ -170,7 +177,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
   if (rc) return rc;
   if ((size_t)B * H * N == 0) return DASH_OK;
-  const Layout L = layout(B, H, N, d);
+  const Layout L = layout(B, H, N, d, resolve(schedule, d, causal));
   if (!workspace || ws_bytes < L.total)
     return fail(DASH_ERR_INVALID_ARG, "workspace missing or smaller than dash_bwd_workspace_size()");
   if (((uintptr_t)workspace & 255) != 0) return fail(DASH_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -255,7 +262,7 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
   if (rc) return rc;
   if ((size_t)B * H * N == 0) return DASH_OK;
   std::lock_guard<std::mutex> lk(g_ws_mu);
-  const size_t need = layout(B, H, N, d).total;
+  const size_t need = layout(B, H, N, d, resolve(schedule, d, causal)).total;
   if (g_ws_bytes < need) {
     if (g_ws) (void)hipFree(g_ws);
     g_ws = nullptr;

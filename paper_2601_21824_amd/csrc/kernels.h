@@ -24,6 +24,11 @@ struct FwdArgs {
   float scale;
 };
 
+// what the main backward kernel does with a KV tile's dQ partial
+constexpr int kModeAtomic = 0;    // fp32 atomic adds into dQacc (non-deterministic comparison)
+constexpr int kModeOrdered = 1;   // the ordered reduction (every DASH schedule)
+constexpr int kModePartials = 2;  // store it in its own buffer; bwd_sum_partials adds them in KV order
+
 struct BwdArgs {
   const void* q;
   const void* k;
@@ -34,7 +39,7 @@ struct BwdArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* dqacc;   // [bh][N][d] fp32 accumulator
+  float* dqacc;   // fp32 accumulator (PARTIALS: one per KV tile)
   float* dvec;    // [bh][N] D = rowsum(dO o O)
   float* lse2;    // [bh][N] L * log2(e)
   int* counters;  // [bh][nblk] ordering counters, kCtrStride ints apart
@@ -42,7 +47,7 @@ struct BwdArgs {
   int32_t* witness;
   float* partials;
   float* dq_accum;
-  int bh, n, nblk, tc;  // tc = real KV tiles per head (ceil(N/d))
+  int bh, n, nblk, tc;  // tc = real KV tiles per head (ceil(N/bc))
   float scale;
   int spin_limit;
   int poison;

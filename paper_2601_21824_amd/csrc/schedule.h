@@ -25,6 +25,8 @@
 //                 visiting order: rank = i-j for i < h; for i >= h,
 //                 (i-h-j) mod h when j < h and j when j >= h.
 //  ATOMIC      -- NAIVE's iteration order, unordered fp32 atomic adds.
+//  PARTIALS    -- NAIVE's iteration order; each partial goes to its own
+//                 buffer and a second kernel sums them in ascending KV order.
 //
 // Padding: with a causal mask every schedule uses br = BC; T_r = g*T_c always
 // (Q tiles past N are empty and skipped); SYMSHIFT rounds T up to even with an
@@ -39,7 +41,8 @@
 
 namespace dash {
 
-enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4 };
+// S_PARTIALS runs NAIVE's chains and writes every partial to its own buffer
+enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4, S_PARTIALS = 6 };
 
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
 constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident

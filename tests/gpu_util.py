@@ -11,12 +11,13 @@ from paper_2601_21824_amd.synth import make_inputs
 REL_FROB = 5e-3
 REL_MAX = 2e-2
 
-FULL_SCHEDULES = ("atomic", "naive", "descending", "shift")
-CAUSAL_SCHEDULES = ("atomic", "naive", "descending", "symshift")
+FULL_SCHEDULES = ("atomic", "naive", "descending", "shift", "partials")
+CAUSAL_SCHEDULES = ("atomic", "naive", "descending", "symshift", "partials")
 
 
-def schedules(causal):
-    return CAUSAL_SCHEDULES if causal else FULL_SCHEDULES
+def schedules(causal, d=128):
+    s = CAUSAL_SCHEDULES if causal else FULL_SCHEDULES
+    return tuple(x for x in s if x != "partials" or d <= 128)
 
 
 def errors(got, ref):

@@ -55,6 +55,20 @@ def test_naive_and_descending_give_identical_dq(N, d):
     assert torch.equal(dq1.view(torch.int16), dq2.view(torch.int16))
 
 
+@pytest.mark.parametrize("N,d,causal", [(1024, 64, True), (333, 64, False), (2048, 128, False), (1000, 128, True)])
+def test_partials_variant_equals_naive_bitwise(N, d, causal):
+    """The materialized-partials comparison variant sums the same partials in
+    the same (ascending KV) order as NAIVE's counters: identical dQ, and dK,
+    dV identical too (same chains)."""
+    B, H = 2, 3
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=19)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, "naive")
+    got = run_bwd(qg, kg, vg, og, dog, lseg, causal, "partials")
+    for a_, b_ in zip(ref, got):
+        assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+
+
 PROTO_CASES = [
     (1, 2, 512, 128, False, "shift"),
     (1, 2, 512, 128, False, "naive"),

@@ -57,7 +57,7 @@ def test_backward_all_schedules_match_oracle(case):
     og, lseg = run_fwd(qg, kg, vg, causal)
     assert_close("O", og, ref_o)
     np.testing.assert_allclose(lseg.cpu().double().numpy(), ref_l, rtol=2e-5, atol=2e-5)
-    for sched in schedules(causal):
+    for sched in schedules(causal, d):
         print(f"  schedule={sched}", flush=True)
         dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
         for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
