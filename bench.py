@@ -56,8 +56,10 @@ class HipEvents:
 def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
     import torch
     q, k, v, o, do, lse, dq, dk, dv, ws = tensors
-    for _ in range(warmup):
+    for _ in range(warmup):  # each warm-up call is checked (the check synchronizes)
         dash.dash_attn_bwd(q, k, v, o, do, lse, dq, dk, dv, causal, sched, workspace=ws)
+        if dash.dash_bwd_check(ws) != dash.DASH_OK:
+            raise RuntimeError(f"{sched}: ordering wait timed out (warm-up)")
     pairs = [(ev.create(), ev.create()) for _ in range(steps)]
     opts = [dash.dash_bwd_options_t(0, 0, None, None, None, a.value, b.value) for a, b in pairs]
     torch.cuda.synchronize()

@@ -63,7 +63,12 @@ typedef enum {
      a second kernel sums the partials of each dQ tile in ascending KV order.
      dQ is bitwise equal to NAIVE's; the workspace holds all T_c partials
      (dash_bwd_workspace_size grows by a factor T_c).  d = 64 and 128. */
-  DASH_SCHED_PARTIALS = 6
+  DASH_SCHED_PARTIALS = 6,
+  /* Comparison point (the same related-work paragraph): two passes, no
+     cross-workgroup reduction -- dK, dV with NAIVE's chains and no dQ work,
+     then a Q-block-parallel dQ kernel that recomputes S and dP and reads K, V
+     again.  d = 64 and 128. */
+  DASH_SCHED_SPLIT = 7
 } dash_schedule_t;
 
 typedef enum {

@@ -17,8 +17,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdash.so")
 
 DASH_SCHED_ATOMIC, DASH_SCHED_NAIVE, DASH_SCHED_DESCENDING = 0, 1, 2
-DASH_SCHED_SHIFT, DASH_SCHED_SYMSHIFT, DASH_SCHED_AUTO, DASH_SCHED_PARTIALS = 3, 4, 5, 6
-SCHEDULES = {"atomic": 0, "naive": 1, "descending": 2, "shift": 3, "symshift": 4, "auto": 5, "partials": 6}
+DASH_SCHED_SHIFT, DASH_SCHED_SYMSHIFT, DASH_SCHED_AUTO, DASH_SCHED_PARTIALS, DASH_SCHED_SPLIT = 3, 4, 5, 6, 7
+SCHEDULES = {"atomic": 0, "naive": 1, "descending": 2, "shift": 3, "symshift": 4, "auto": 5, "partials": 6,
+             "split": 7}
 DASH_OK, DASH_ERR_INVALID_ARG, DASH_ERR_UNSUPPORTED = 0, -1, -2
 DASH_ERR_HIP, DASH_ERR_TIMEOUT, DASH_ERR_NO_DEVICE = -3, -4, -5
 DASH_FLAG_POISON_COUNTERS = 1

@@ -10,12 +10,13 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdash.so")
-SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd256.hip", "dash_api.hip"]
+SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd256.hip", "attn_dq.hip", "dash_api.hip"]
 HEADERS = ["common.h", "kernels.h", "schedule.h"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-    # no packed-fp32 instructions (correctness on this fleet)
+    # no packed-fp32 (v_pk_*_f32) instructions: some of their forms have given
+    # silently wrong results on this hardware
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
 ]

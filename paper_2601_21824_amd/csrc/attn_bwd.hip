@@ -12,7 +12,7 @@
 //              dV += P^T dO, dK += dS^T Q          (P^T, dS^T fed from registers)
 //              dQ^T_loc = K^T dS^T                 (dS staged through LDS)
 //            then the ordered reduction (Algorithm 1, the dQ writer): wait until
-//            the block's counter equals this tile's rank, add the partial into
+//            the block's counter has reached this tile's rank, add the partial into
 //            the fp32 dQ accumulator with device-coherent (SC1) loads/stores, make
 //            the stores visible, bump the counter.  The last rank writes bf16
 //            s*dQ directly.  No atomics touch the data; the order is fixed by the
@@ -64,6 +64,38 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a, int zero_acc) {
   if (gtid == 0) {
     a.ctrl[kCtrlTicket] = 0;
     a.ctrl[kCtrlError] = 0;
+  }
+  // every chain's step table (the same for every head): entry 0 is the number
+  // of steps; entry 1 + st is step st, i.e. 64-row block pb of Q tile i with
+  // KV tile j, its rank in the block's summation order and whether it is the
+  // last one (see pack_step)
+  {
+    const Geom& G = a.G;
+    const int bc = G.bc;
+    const long ntab = (long)G.chains * a.step_cap;
+    for (long x = gtid; x < ntab; x += nthreads) {
+      const int w = (int)(x / a.step_cap), e = (int)(x % a.step_cap);
+      const int len = chain_len(G, w) * G.nsub;
+      if (e == 0) {
+        a.steps[x] = (unsigned)len;
+        continue;
+      }
+      const int st = e - 1;
+      if (st >= len) continue;
+      int j, i;
+      task(G, w, st / G.nsub, &j, &i);
+      const int pb = i * G.nsub + st % G.nsub;
+      const int rank = rank_of(G, i, j);
+      a.steps[x] = (pb * kBlockRows < a.n && j * bc < a.n) ? pack_step(pb, j, rank, rank == contributors(G, i) - 1) : kNoStep;
+    }
+    // work ticket -> (head, chain)
+    const long nitems = (long)a.bh * G.chains;
+    for (long x = gtid; x < nitems; x += nthreads) {
+      int bh, w;
+      ticket_chain(G, a.bh, (int)x, &bh, &w);
+      a.order[2 * x] = bh;
+      a.order[2 * x + 1] = w;
+    }
   }
   if (zero_acc) {
     const long n4 = (long)a.bh * a.n * D / 4;
@@ -187,9 +219,12 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(&a.ctrl[kCtrlTicket], 1);
     __syncthreads();
-    const int item = sm.item;
+    const int item = __builtin_amdgcn_readfirstlane(sm.item);  // wave-uniform (SGPR)
     if (item >= total) break;
-    const int bh = item / G.chains, wch = item % G.chains;
+    // (head, chain) of the ticket from bwd_pre's table; wave-uniform, so the
+    // head's buffer descriptors stay in SGPRs
+    const int bh = __builtin_amdgcn_readfirstlane(a.order[2 * item]);
+    const int wch = __builtin_amdgcn_readfirstlane(a.order[2 * item + 1]);
     const size_t head = (size_t)bh * N * D;
     const auto rq = make_rsrc((const __bf16*)a.q + head, hbytes);
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
@@ -198,16 +233,11 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     const auto racc = make_rsrc(a.dqacc + (size_t)bh * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
 
-    const int nsteps = chain_len(G, wch) * G.nsub;
-    // the chain's schedule, computed once into LDS (the previous chain's
-    // readers all passed the barrier after the ticket)
-    for (int st = tid; st < nsteps; st += NT) {
-      int j, i;
-      task(G, wch, st / G.nsub, &j, &i);
-      const int pb = i * G.nsub + st % G.nsub;
-      sm.steps[st] = (pb * BM < N && j * BC < N) ? pack_step(pb, j, rank_of(G, i, j), rank_of(G, i, j) == contributors(G, i) - 1)
-                                                 : kNoStep;
-    }
+    const unsigned* tab = a.steps + (size_t)wch * a.step_cap;
+    const int nsteps = __builtin_amdgcn_readfirstlane((int)tab[0]);
+    // the chain's schedule (computed by bwd_pre) into LDS; the previous
+    // chain's readers all passed the barrier after the ticket
+    for (int st = tid; st < nsteps; st += NT) sm.steps[st] = tab[1 + st];
     __syncthreads();
     int cur_j = -1;
     bf16x8 kreg[KS], vreg[KS], ktreg[KSC];  // K, V rows (B of S = Q K^T, dP = dO V^T), K^T (A of dQ^T = K^T dS^T)
@@ -452,7 +482,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       //      during the next run so its latency hides behind the MFMAs
       if (ordered && !failed) {
         const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
-        if (v0 == NW * rank) {
+        if (v0 >= NW * rank) {
           have_turn = true;
           __atomic_signal_fence(__ATOMIC_SEQ_CST);
         }
@@ -474,8 +504,10 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       });
       // run 4: dV/dK of half 1, with the dS^T stores
       dvdk(1, [&](int k) {
+        if constexpr (MODE != kModeNoDq) {
 #pragma unroll
-        for (int p = k * 8 / (2 * NB); p < (k + 1) * 8 / (2 * NB); ++p) store_ds_piece(p);
+          for (int p = k * 8 / (2 * NB); p < (k + 1) * 8 / (2 * NB); ++p) store_ds_piece(p);
+        }
       });
 
       // deferred release of the previous block: when this step prefetched,
@@ -490,126 +522,131 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         release();
       }
-      __syncthreads();
+      if constexpr (MODE == kModeNoDq) {
+        // dK, dV only: the next block's Q / dO have landed before the barrier
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      } else {
+        __syncthreads();
 
-      // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T,
-      //      k-step ks reads A = K^T (shared by both query halves) and two B's
-      f32x16 dq[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) dq[qb][r] = 0.f;
-      {
-        constexpr int RING = 3;
-        auto rd = [&](int ks, bf16x8* b0, bf16x8* b1) {
-          const int krow = 16 * ks + 8 * g + (L16 >> 2);
-          const int qc0 = 16 * nh + 4 * (L16 & 3), qc1 = 32 + qc0;
-          *b0 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc0)]), tr_read(&sm.dst[dst_at(krow + 4, qc0)]));
-          *b1 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc1)]), tr_read(&sm.dst[dst_at(krow + 4, qc1)]));
-        };
-        bf16x8 rb0[RING], rb1[RING];
-#pragma unroll
-        for (int k = 0; k < RING; ++k) rd(k, &rb0[k], &rb1[k]);
-#pragma unroll
-        for (int ks = 0; ks < KSC; ++ks) {
-          __builtin_amdgcn_sched_barrier(0);
-          dq[0] = mfma32(ktreg[ks], rb0[ks % RING], dq[0]);
-          dq[1] = mfma32(ktreg[ks], rb1[ks % RING], dq[1]);
-          if (ks + RING < KSC) rd(ks + RING, &rb0[ks % RING], &rb1[ks % RING]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      // dq[qb][r] <-> query 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
-
-      if (a.partials) {
-        const auto rp = make_rsrc(a.partials + ((size_t)bh * a.tc + j) * N * D, hbytes * 2);
-#pragma unroll
+        // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T,
+        //      k-step ks reads A = K^T (shared by both query halves) and two B's
+        f32x16 dq[2];
+  #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
-            st16(rp, (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g) * 4,
-                 __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
-      }
-
-      bool add = false;  // accumulate into the slice (else: the partial is stored as is)
-      if (ordered) {
-        if (!have_turn && !failed) {
-          have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
-          if (!have_turn) {
-            failed = true;
-            __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          } else if (rank > 0) {
-            load_acc(pb);  // late fetch: the turn came after the early poll
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) dq[qb][r] = 0.f;
+        {
+          constexpr int RING = 3;
+          auto rd = [&](int ks, bf16x8* b0, bf16x8* b1) {
+            const int krow = 16 * ks + 8 * g + (L16 >> 2);
+            const int qc0 = 16 * nh + 4 * (L16 & 3), qc1 = 32 + qc0;
+            *b0 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc0)]), tr_read(&sm.dst[dst_at(krow + 4, qc0)]));
+            *b1 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc1)]), tr_read(&sm.dst[dst_at(krow + 4, qc1)]));
+          };
+          bf16x8 rb0[RING], rb1[RING];
+  #pragma unroll
+          for (int k = 0; k < RING; ++k) rd(k, &rb0[k], &rb1[k]);
+  #pragma unroll
+          for (int ks = 0; ks < KSC; ++ks) {
+            __builtin_amdgcn_sched_barrier(0);
+            dq[0] = mfma32(ktreg[ks], rb0[ks % RING], dq[0]);
+            dq[1] = mfma32(ktreg[ks], rb1[ks % RING], dq[1]);
+            if (ks + RING < KSC) rd(ks + RING, &rb0[ks % RING], &rb1[ks % RING]);
           }
+          __builtin_amdgcn_sched_barrier(0);
         }
-        add = have_turn && rank > 0;
-      }
-      // this wave's slice (and the next block's Q / dO) have landed
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      // sample the next block's counter now, ahead of the stores below
-      if (ordered && pb_next >= 0)
-        poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if constexpr (ordered) {
-        // ---- add this wave's partial into its slice straight from registers:
-        //      the accumulator is stored in this wave's register order, so the
-        //      slice arrives (LDS landing pad) and leaves in 1 KB coalesced rows.
-        //      Each element is touched by exactly one lane: the sum order is the
-        //      schedule's.
-        if (have_turn) {
-          const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
-          f32x4 old[8];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const int qb = k >> 2, rb = k & 3;
-            f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
-            const f32x4 sum = old[k] + v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
-            if (last) {
-              const uint32_t off = (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g);
-              st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
-              if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
-            } else {
-              st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+        // dq[qb][r] <-> query 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
+
+        if (a.partials) {
+          const auto rp = make_rsrc(a.partials + ((size_t)bh * a.tc + j) * N * D, hbytes * 2);
+  #pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+  #pragma unroll
+            for (int rb = 0; rb < 4; ++rb)
+              st16(rp, (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g) * 4,
+                   __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+        }
+
+        bool add = false;  // accumulate into the slice (else: the partial is stored as is)
+        if (ordered) {
+          if (!have_turn && !failed) {
+            have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
+            if (!have_turn) {
+              failed = true;
+              __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else if (rank > 0) {
+              load_acc(pb);  // late fetch: the turn came after the early poll
             }
           }
+          add = have_turn && rank > 0;
         }
-      } else if constexpr (MODE == kModePartials) {
-        // ---- partials variant: the partial goes to KV tile j's own buffer, in
-        //      the same register order as the ordered accumulator
-        const auto rpb = make_rsrc(a.dqacc + ((size_t)bh * a.tc + j) * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int qb = k >> 2, rb = k & 3;
-          st16(rpb, acc_off(pb, k), __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+        // this wave's slice (and the next block's Q / dO) have landed
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // sample the next block's counter now, ahead of the stores below
+        if (ordered && pb_next >= 0)
+          poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (ordered) {
+          // ---- add this wave's partial into its slice straight from registers:
+          //      the accumulator is stored in this wave's register order, so the
+          //      slice arrives (LDS landing pad) and leaves in 1 KB coalesced rows.
+          //      Each element is touched by exactly one lane: the sum order is the
+          //      schedule's.
+          if (have_turn) {
+            const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
+            f32x4 old[8];
+  #pragma unroll
+            for (int k = 0; k < 8; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+  #pragma unroll
+            for (int k = 0; k < 8; ++k) {
+              const int qb = k >> 2, rb = k & 3;
+              f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+              const f32x4 sum = old[k] + v;
+  #pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
+              if (last) {
+                const uint32_t off = (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g);
+                st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
+                if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
+              } else {
+                st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+              }
+            }
+          }
+        } else if constexpr (MODE == kModePartials) {
+          // ---- partials variant: the partial goes to KV tile j's own buffer, in
+          //      the same register order as the ordered accumulator
+          const auto rpb = make_rsrc(a.dqacc + ((size_t)bh * a.tc + j) * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
+  #pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int qb = k >> 2, rb = k & 3;
+            st16(rpb, acc_off(pb, k), __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+          }
+        } else {
+          // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
+          //      atomic per element, each instruction covering two whole 128-byte
+          //      row segments of the row-major dQacc
+  #pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
+            *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] =
+                f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+          }
+          asm volatile("" ::: "memory");  // lanes read what other lanes wrote
+          const int c = l & 31;
+  #pragma unroll 8
+          for (int k = 0; k < 32; ++k) {
+            const int q = 2 * k + (l >> 5);
+            const float v = acc_w[(q * 8 + ((c >> 2) ^ (q & 7))) * 4 + (c & 3)];
+            if (q0 + q < N) atomicAdd(a.dqacc + head + (size_t)(q0 + q) * D + 32 * w + c, v);
+          }
         }
-      } else {
-        // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
-        //      atomic per element, each instruction covering two whole 128-byte
-        //      row segments of the row-major dQacc
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
-          *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] =
-              f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
-        }
-        asm volatile("" ::: "memory");  // lanes read what other lanes wrote
-        const int c = l & 31;
-#pragma unroll 8
-        for (int k = 0; k < 32; ++k) {
-          const int q = 2 * k + (l >> 5);
-          const float v = acc_w[(q * 8 + ((c >> 2) ^ (q & 7))) * 4 + (c & 3)];
-          if (q0 + q < N) atomicAdd(a.dqacc + head + (size_t)(q0 + q) * D + 32 * w + c, v);
-        }
-      }
-      if (ordered) {
-        if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
-        pend_ctr = pb;
-        if (!deferred || nst >= nsteps) {
-          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-          release();
+        if (ordered) {
+          if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
+          pend_ctr = pb;
+          if (!deferred || nst >= nsteps) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            release();
+          }
         }
       }
       buf ^= 1;
@@ -627,6 +664,8 @@ void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeAtomic>), grid, block, 0, stream, a);
   else if (a.G.sched == S_PARTIALS)
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModePartials>), grid, block, 0, stream, a);
+  else if (a.G.sched == S_SPLIT)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeNoDq>), grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered>), grid, block, 0, stream, a);
 }
@@ -650,8 +689,10 @@ void launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t st
     launch_main<D>(a, grid_main, stream);
   if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
   if (atomic) hipLaunchKernelGGL(bwd_post_kernel<D>, dim3(1024), dim3(256), 0, stream, a);
-  if constexpr (D <= 128)
+  if constexpr (D <= 128) {
     if (a.G.sched == S_PARTIALS) hipLaunchKernelGGL(bwd_sum_partials_kernel<D>, dim3(4096), dim3(256), 0, stream, a);
+    if (a.G.sched == S_SPLIT) (void)launch_dq(a, D, stream);
+  }
 }
 
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream) {
@@ -672,9 +713,10 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 template <int D>
 int main_occupancy() {
   int lo = 1 << 30;
-  const void* fns[6] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
-                        (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeAtomic>,
-                        (const void*)bwd_main_kernel<D, true, kModeOrdered>, (const void*)bwd_main_kernel<D, true, kModePartials>};
+  const void* fns[8] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
+                        (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, false, kModeNoDq>,
+                        (const void*)bwd_main_kernel<D, true, kModeAtomic>, (const void*)bwd_main_kernel<D, true, kModeOrdered>,
+                        (const void*)bwd_main_kernel<D, true, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeNoDq>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 2 * D, 0) != hipSuccess) return 0;

@@ -88,9 +88,12 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(&a.ctrl[kCtrlTicket], 1);
     __syncthreads();
-    const int item = sm.item;
+    const int item = __builtin_amdgcn_readfirstlane(sm.item);  // wave-uniform (SGPR)
     if (item >= total) break;
-    const int bh = item / G.chains, wch = item % G.chains;
+    // (head, chain) of the ticket from bwd_pre's table; wave-uniform, so the
+    // head's buffer descriptors stay in SGPRs
+    const int bh = __builtin_amdgcn_readfirstlane(a.order[2 * item]);
+    const int wch = __builtin_amdgcn_readfirstlane(a.order[2 * item + 1]);
     const size_t head = (size_t)bh * N * D;
     const auto rq = make_rsrc((const __bf16*)a.q + head, hbytes);
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
@@ -99,14 +102,10 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
     const auto racc = make_rsrc(a.dqacc + (size_t)bh * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
 
-    const int nsteps = chain_len(G, wch) * G.nsub;
-    for (int st = tid; st < nsteps; st += NT) {
-      int j, i;
-      task(G, wch, st / G.nsub, &j, &i);
-      const int pb = i * G.nsub + st % G.nsub;
-      sm.steps[st] = (pb * BM < N && j * BC < N) ? pack_step(pb, j, rank_of(G, i, j), rank_of(G, i, j) == contributors(G, i) - 1)
-                                                 : kNoStep;
-    }
+    const unsigned* tab = a.steps + (size_t)wch * a.step_cap;
+    const int nsteps = __builtin_amdgcn_readfirstlane((int)tab[0]);
+    // the chain's schedule (computed by bwd_pre) into LDS
+    for (int st = tid; st < nsteps; st += NT) sm.steps[st] = tab[1 + st];
     __syncthreads();
 
     int cur_j = -1;
@@ -255,7 +254,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
       //      if the turn is ours, fetch the accumulator slice now
       if (ordered && !failed) {
         const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
-        if (v0 == NW * rank) {
+        if (v0 >= NW * rank) {
           have_turn = true;
           __atomic_signal_fence(__ATOMIC_SEQ_CST);
           if (rank > 0) load_acc(pb);

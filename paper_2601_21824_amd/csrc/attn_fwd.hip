@@ -22,7 +22,8 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdArgs a) {
   __shared__ __attribute__((aligned(16))) __bf16 VTs[D * KB];
 
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, g = l >> 5, lc = l & 31;
-  const int bh = blockIdx.y, q0 = blockIdx.x * 128, N = a.n;
+  // causal: the longest query blocks (last rows) are dispatched first
+  const int bh = blockIdx.y, q0 = (a.causal ? gridDim.x - 1 - blockIdx.x : blockIdx.x) * 128, N = a.n;
   const size_t head = (size_t)bh * N * D;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   const auto rq = make_rsrc((const __bf16*)a.q + head, hbytes);

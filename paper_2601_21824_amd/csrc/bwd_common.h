@@ -8,14 +8,18 @@
 namespace dash {
 
 // ---------------------------------------------------------------- ordering
-// Spin until *ctr == want (relaxed, device-coherent loads).  Wave-uniform.
+// Spin until *ctr >= want (relaxed, device-coherent loads).  Wave-uniform.
 // A block's counter advances by one per wave of each contributor, so rank r
-// holds the turn when it reads (waves per workgroup) * r.
+// holds the turn once it reads at least (waves per workgroup) * r.  The test
+// is "at least", not "equal": the other waves of the same workgroup share the
+// rank and bump the counter as soon as their own slices are stored, so a wave
+// that polls late sees up to waves - 1 more; it cannot see (waves) * (r + 1),
+// which needs its own bump.
 // Returns false after `limit` polls; the caller then skips its update.
 __device__ inline bool wait_turn(const int* ctr, int want, int limit) {
   for (int n = 0;; ++n) {
     const int v = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    if (v == want) break;
+    if (v >= want) break;
     if (n >= limit) return false;
     __builtin_amdgcn_s_sleep(2);
   }

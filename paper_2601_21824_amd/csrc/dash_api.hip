@@ -28,7 +28,8 @@ int hip_fail(hipError_t e, const char* what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ctrl, dqacc, dvec, lse2, counters, total;
+  size_t ctrl, dqacc, dvec, lse2, counters, steps, order, total;
+  int step_cap;
 };
 
 // ctrl first so that dash_bwd_check can find it without the problem size.
@@ -51,6 +52,17 @@ Layout layout(int B, int H, int N, int d, int sched) {
   off += align256(bh * N * sizeof(float));
   L.counters = off;
   off += align256(bh * nblk * dash::kCtrStride * sizeof(int));
+  // per-chain step tables: at most T_c + 1 chains (Symmetric Shift pads T_c),
+  // each its length and at most (T_r + 1) * nsub steps; then the ticket order
+  const dash::Geom G = dash::make_geom(sched, 0, N, d);
+  const dash::Geom Gc = dash::make_geom(sched, 1, N, d);
+  const int cap_f = (G.t_r + 1) * G.nsub, cap_c = (Gc.t_r + 1) * Gc.nsub;
+  L.step_cap = 1 + (cap_f > cap_c ? cap_f : cap_c);
+  const size_t chains = (size_t)(G.t_c > Gc.t_c ? G.t_c : Gc.t_c) + 1;
+  L.steps = off;
+  off += align256(chains * L.step_cap * sizeof(unsigned));
+  L.order = off;
+  off += align256(bh * chains * 2 * sizeof(int));
   L.total = off;
   return L;
 }
@@ -108,7 +120,7 @@ int resolve(int schedule, int d, int causal) {
 }
 
 int check_schedule(int schedule, int causal) {
-  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_PARTIALS)
+  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_SPLIT)
     return fail(DASH_ERR_INVALID_ARG, "unknown schedule");
   if (schedule == DASH_SCHED_SYMSHIFT && !causal)
     return fail(DASH_ERR_UNSUPPORTED, "symmetric shift is the causal-mask schedule; use SHIFT for a full mask");
@@ -122,8 +134,8 @@ int check_bwd(const void* q, const void* k, const void* v, const void* o, const 
   int rc = check_shape(B, H, N, d);
   if (rc) return rc;
   if ((rc = check_schedule(schedule, causal))) return rc;
-  if (schedule == DASH_SCHED_PARTIALS && d > 128)
-    return fail(DASH_ERR_UNSUPPORTED, "the partials comparison variant is built for d = 64 and 128");
+  if ((schedule == DASH_SCHED_PARTIALS || schedule == DASH_SCHED_SPLIT) && d > 128)
+    return fail(DASH_ERR_UNSUPPORTED, "the partials and split comparison variants are built for d = 64 and 128");
   if ((size_t)B * H * N == 0) return DASH_OK;
   if (!q || !k || !v || !o || !dO || !lse || !dq || !dk || !dv)
     return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
@@ -145,7 +157,7 @@ int dash_resolve_schedule(int schedule, int d, int causal) { return resolve(sche
 
 size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule) {
   if (check_shape(B, H, N, d) != DASH_OK) return 0;
-  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_PARTIALS) return 0;
+  if (schedule < DASH_SCHED_ATOMIC || schedule > DASH_SCHED_SPLIT) return 0;
   return layout(B, H, N, d, resolve(schedule, d, 0)).total;
 }
 
@@ -224,6 +236,9 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   a.lse2 = (float*)(ws + L.lse2);
   a.counters = (int*)(ws + L.counters);
   a.ctrl = (int*)(ws + L.ctrl);
+  a.steps = (unsigned*)(ws + L.steps);
+  a.step_cap = L.step_cap;
+  a.order = (int*)(ws + L.order);
   a.witness = opts ? opts->witness : nullptr;
   a.partials = opts ? opts->partials : nullptr;
   a.dq_accum = opts ? opts->dq_accum : nullptr;

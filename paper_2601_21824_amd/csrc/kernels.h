@@ -8,7 +8,7 @@
 namespace dash {
 
 constexpr int kCtrStride = 32;        // ints per ordering counter (one 128-byte line each)
-constexpr int kPoison = 0x40000000;   // counter start value no rank waits for
+constexpr int kPoison = -0x40000000;  // counter start value below every rank's turn
 constexpr int kCtrlTicket = 0;        // ctrl[] slot: next work item
 constexpr int kCtrlError = 16;        // ctrl[] slot: set to 1 when a wait timed out
 constexpr size_t kCtrlBytes = 256;    // ctrl block at the start of the workspace
@@ -28,6 +28,7 @@ struct FwdArgs {
 constexpr int kModeAtomic = 0;    // fp32 atomic adds into dQacc (non-deterministic comparison)
 constexpr int kModeOrdered = 1;   // the ordered reduction (every DASH schedule)
 constexpr int kModePartials = 2;  // store it in its own buffer; bwd_sum_partials adds them in KV order
+constexpr int kModeNoDq = 3;      // no dQ at all: dK, dV only (SPLIT's first pass)
 
 struct BwdArgs {
   const void* q;
@@ -44,6 +45,9 @@ struct BwdArgs {
   float* lse2;    // [bh][N] L * log2(e)
   int* counters;  // [bh][nblk] ordering counters, kCtrStride ints apart
   int* ctrl;      // ticket / error flag
+  unsigned* steps;  // [chains][step_cap]: per chain its length, then its packed steps (bwd_pre writes them)
+  int step_cap;
+  int* order;       // [bh * chains][2]: work ticket -> (head, chain) (bwd_pre writes it)
   int32_t* witness;
   float* partials;
   float* dq_accum;
@@ -57,6 +61,7 @@ struct BwdArgs {
 
 hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream);
+hipError_t launch_dq(const BwdArgs& a, int d, hipStream_t stream);  // SPLIT's dQ pass (attn_dq.hip)
 int bwd_main_occupancy(int d);
 // head dim 256 (attn_bwd256.hip)
 void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream);

@@ -42,7 +42,8 @@
 namespace dash {
 
 // S_PARTIALS runs NAIVE's chains and writes every partial to its own buffer
-enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4, S_PARTIALS = 6 };
+// S_SPLIT runs NAIVE's chains for dK, dV only; dQ is a separate pass
+enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4, S_PARTIALS = 6, S_SPLIT = 7 };
 
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
 constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident
@@ -133,6 +134,22 @@ DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
       *j = w;
       *i = first_q(G, w) + t;
       return;
+  }
+}
+
+// Work ticket -> (head, chain).  Head-major by default (all chains of a head
+// in a row, as Shift and Symmetric Shift need them together).  With a causal
+// mask, the schedules whose waits only point to lower KV tiles go chain-major
+// instead: chain w of every head before chain w+1, i.e. the longest chains
+// first across heads (longest-processing-time order); every chain a wait
+// points to still has a lower ticket.
+DASH_HD void ticket_chain(const Geom& G, int heads, int item, int* bh, int* w) {
+  if (G.causal && G.sched != S_SYMSHIFT && G.sched != S_SHIFT) {
+    *w = item / heads;
+    *bh = item % heads;
+  } else {
+    *bh = item / G.chains;
+    *w = item % G.chains;
   }
 }
 

@@ -11,13 +11,13 @@ from paper_2601_21824_amd.synth import make_inputs
 REL_FROB = 5e-3
 REL_MAX = 2e-2
 
-FULL_SCHEDULES = ("atomic", "naive", "descending", "shift", "partials")
-CAUSAL_SCHEDULES = ("atomic", "naive", "descending", "symshift", "partials")
+FULL_SCHEDULES = ("atomic", "naive", "descending", "shift", "partials", "split")
+CAUSAL_SCHEDULES = ("atomic", "naive", "descending", "symshift", "partials", "split")
 
 
 def schedules(causal, d=128):
     s = CAUSAL_SCHEDULES if causal else FULL_SCHEDULES
-    return tuple(x for x in s if x != "partials" or d <= 128)
+    return tuple(x for x in s if x not in ("partials", "split") or d <= 128)
 
 
 def errors(got, ref):
@@ -51,7 +51,7 @@ def run_fwd(qg, kg, vg, causal):
 def run_bwd(qg, kg, vg, og, dog, lseg, causal, schedule, options=None, workspace=None):
     B, H, N, d = qg.shape
     if options is not None and workspace is None:
-        workspace = dash.new_workspace(B, H, N, d)
+        workspace = dash.new_workspace(B, H, N, d, schedule)
     dq, dk, dv = dash.attn_bwd(qg, kg, vg, og, dog, lseg, causal, schedule, workspace=workspace,
                                options=options)
     torch.cuda.synchronize()

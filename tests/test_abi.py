@@ -54,6 +54,8 @@ def test_argument_errors_without_device():
     base = b.dash_bwd_workspace_size(2, 16, 8192, 128, "naive")
     assert b.dash_bwd_workspace_size(2, 16, 8192, 128, "partials") >= base + 63 * 2 * 16 * 8192 * 128 * 4
     assert call_bwd(lib, 4096, d=256, sched=b.DASH_SCHED_PARTIALS) == b.DASH_ERR_UNSUPPORTED
+    assert call_bwd(lib, 4096, d=256, sched=b.DASH_SCHED_SPLIT) == b.DASH_ERR_UNSUPPORTED
+    assert call_bwd(lib, 4096, sched=8) == b.DASH_ERR_INVALID_ARG
     assert lib.dash_bwd_check(ctypes.c_void_p(0), ctypes.c_void_p(0)) == b.DASH_ERR_INVALID_ARG
     # explicit-workspace form: too small a workspace is an argument error
     opts = b.dash_bwd_options_t(0, 0, None, None, None, None, None)
@@ -75,13 +77,14 @@ def test_schedule_resolution():
 
 KINDS = {b.DASH_SCHED_NAIVE: osched.NAIVE, b.DASH_SCHED_DESCENDING: osched.DESCENDING,
          b.DASH_SCHED_SHIFT: osched.SHIFT, b.DASH_SCHED_SYMSHIFT: osched.SYMSHIFT,
-         b.DASH_SCHED_ATOMIC: osched.NAIVE, b.DASH_SCHED_PARTIALS: osched.NAIVE}
+         b.DASH_SCHED_ATOMIC: osched.NAIVE, b.DASH_SCHED_PARTIALS: osched.NAIVE,
+         b.DASH_SCHED_SPLIT: osched.NAIVE}
 
 
 @pytest.mark.parametrize("d", [64, 128, 256])
 @pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 8192, 16384, 32768])
 @pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("sched", [0, 1, 2, 3, 4, 6])
+@pytest.mark.parametrize("sched", [0, 1, 2, 3, 4, 6, 7])
 def test_schedule_table_matches_oracle(sched, causal, N, d):
     if sched == b.DASH_SCHED_SYMSHIFT and not causal:
         pytest.skip("symshift is causal-only")

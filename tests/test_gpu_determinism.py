@@ -24,6 +24,8 @@ DET_CASES = [
     (2, 4, 2048, 128, True, "symshift"),
     (1, 2, 1024, 256, False, "shift"),
     (1, 2, 1024, 256, True, "symshift"),
+    (2, 4, 2048, 128, True, "split"),
+    (2, 4, 2048, 128, False, "partials"),
 ]
 
 
@@ -33,7 +35,7 @@ def test_bitwise_identical_over_100_runs(case):
     print(f"\n[determinism] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=77)
     og, lseg = run_fwd(qg, kg, vg, causal)
-    ws = dash.new_workspace(B, H, N, d)
+    ws = dash.new_workspace(B, H, N, d, sched)
     first = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
     outs = [torch.empty_like(t) for t in first]
     for r in range(99):
@@ -42,6 +44,38 @@ def test_bitwise_identical_over_100_runs(case):
         for a, b in zip(first, outs):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"run {r + 2} differs"
     assert dash.dash_bwd_check(ws) == dash.DASH_OK
+
+
+SERIAL_CASES = [
+    (1, 8, 32768, 256, False, "naive"),
+    (1, 8, 32768, 256, False, "descending"),
+    (1, 8, 32768, 256, True, "naive"),
+    (1, 8, 32768, 256, True, "descending"),
+    (1, 16, 16384, 128, True, "naive"),
+]
+
+
+@pytest.mark.parametrize("case", SERIAL_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in SERIAL_CASES])
+def test_serialized_schedules_never_miss_a_turn(case):
+    """Naive and Descending wait at almost every step, with more chains than
+    resident workgroups at these lengths.  All waves of a workgroup share the
+    contributor's rank and each bumps the counter after its own slice, so a
+    wave that polls after a sibling's bump must still take its turn: every call
+    completes without a wait timeout and gives the same bits."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[serialized] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=5, sigma=0.5)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d, sched)
+    opts = dash.dash_bwd_options_t(1 << 20, 0, None, None, None, None, None, 0)
+    first = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts)
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    outs = [torch.empty_like(t) for t in first]
+    for r in range(7):
+        dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, *outs, causal, sched, workspace=ws, options=opts)
+        assert dash.dash_bwd_check(ws) == dash.DASH_OK, f"call {r + 2} timed out"
+        for a, b in zip(first, outs):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"call {r + 2} differs"
 
 
 @pytest.mark.parametrize("N,d", [(1024, 64), (2048, 128)])
