@@ -111,8 +111,11 @@ def cpu_baseline(q, k, v, do, causal, flops_per_head):
 def sweep(dash, make_inputs, args):
     import torch
     ev = HipEvents()
-    cases = [(16384 // n, 16, n, 128, False) for n in (512, 1024, 2048, 4096, 8192, 16384)]
-    cases += [(16384 // n, 32, n, 128, True) for n in (512, 1024, 2048, 4096, 8192, 16384)]
+    ns = (512, 1024, 2048, 4096, 8192, 16384)
+    cases = [(16384 // n, 16, n, 128, False) for n in ns]
+    cases += [(16384 // n, 32, n, 128, True) for n in ns]
+    cases += [(16384 // n, 32, n, 64, False) for n in ns]  # head dim 64, hidden 2048
+    cases += [(16384 // n, 32, n, 64, True) for n in ns]
     cases += [(4, 16, 1024, 64, True)]
     cases += [(1, 8, 32768, 256, False), (1, 8, 32768, 256, True)]  # long sequence, head dim 256
     for B, H, N, d, causal in cases:
@@ -121,14 +124,16 @@ def sweep(dash, make_inputs, args):
         qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
         og, lseg = dash.attn_fwd(qg, kg, vg, causal)
         dq, dk, dv = torch.empty_like(qg), torch.empty_like(kg), torch.empty_like(vg)
-        ws = dash.new_workspace(B, H, N, d)
+        scheds = ("descending", "symshift", "naive", "atomic") if causal else ("shift", "descending", "naive", "atomic")
+        if d <= 128:  # the comparison designs are built for d = 64, 128
+            scheds += ("split", "partials")
+        ws = dash.new_workspace(B, H, N, d, "partials" if "partials" in scheds else "shift")
         tensors = (qg, kg, vg, og, dog, lseg, dq, dk, dv, ws)
-        scheds = ("descending", "symshift", "naive", "atomic") if causal else ("shift", "naive", "atomic")
         row = {"B": B, "H": H, "N": N, "d": d, "mask": "causal" if causal else "full"}
         for sched in scheds:
             ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
             row[sched] = round(flops / (ms * 1e-3) / 1e12, 1)
-        det = max(row[s] for s in scheds if s != "atomic")
+        det = max(row[s] for s in scheds if s not in ("atomic", "split", "partials"))
         row["best_det_pct_of_atomic"] = round(100 * det / row["atomic"], 1)
         print(json.dumps(row), flush=True)
         del tensors, qg, kg, vg, dog, og, lseg, dq, dk, dv, ws
@@ -149,9 +154,9 @@ def main():
     ap.add_argument("--schedules", default="",
                     help="comma list of schedules to time (default: the schedule, atomic, naive)")
     ap.add_argument("--sweep", action="store_true",
-                    help="time every schedule over the 16k-token sweeps (full H=16, causal H=32, d=128), "
-                         "the B=4 H=16 N=1024 d=64 causal case and B=1 H=8 N=32768 d=256 (both masks); "
-                         "one JSON line per case")
+                    help="time every schedule over the 16k-token sweeps (d=128: full H=16, causal H=32; "
+                         "d=64: H=32, both masks), the B=4 H=16 N=1024 d=64 causal case and B=1 H=8 "
+                         "N=32768 d=256 (both masks); one JSON line per case")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run 5 plain device copies of this many bytes (counter calibration)")
     args = ap.parse_args()

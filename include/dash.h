@@ -52,11 +52,9 @@ typedef enum {
   /* Symmetric Shift (Section 3.4, causal masks): KV tiles j and T-1-j share a
      workgroup; two-phase fold.  Causal mask only. */
   DASH_SCHED_SYMSHIFT = 4,
-  /* SHIFT for full masks.  Causal masks: SYMSHIFT at d = 64 and 128, where it
-     measures faster here (its schedule lives in an LDS step table, so the
-     register cost that makes the paper prefer DESCENDING at d >= 128, Section
-     4.3, does not arise), DESCENDING at d = 256, where it measures faster on
-     long sequences. */
+  /* SHIFT for full masks, DESCENDING for causal masks (the paper's choice at
+     d >= 128, Section 4.3; on this GPU it also beats SYMSHIFT at d = 64 and
+     on long sequences at every d). */
   DASH_SCHED_AUTO = 5,
   /* Comparison point (related work, "Deterministic Implementations"): every
      KV tile stores its dQ partial in its own fp32 buffer, no ordering waits;

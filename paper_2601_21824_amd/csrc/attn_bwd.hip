@@ -181,6 +181,7 @@ struct MainSmem {
   float ls[2][BM];         // L * log2(e) per query row
   float ds[2][BM];         // D per query row
   unsigned steps[kMaxChainSteps];  // this chain's blocks, see pack_step
+  int poll[D / 32][64];  // per wave: the coming block's counter (direct load, all lanes alike)
   int item;
 };
 
@@ -232,6 +233,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     const auto rdo = make_rsrc((const __bf16*)a.dO + head, hbytes);
     const auto racc = make_rsrc(a.dqacc + (size_t)bh * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
+    const auto rctr = make_rsrc(ctr_head, (uint32_t)a.nblk * kCtrStride * 4);
 
     const unsigned* tab = a.steps + (size_t)wch * a.step_cap;
     const int nsteps = __builtin_amdgcn_readfirstlane((int)tab[0]);
@@ -243,7 +245,12 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     bf16x8 kreg[KS], vreg[KS], ktreg[KSC];  // K, V rows (B of S = Q K^T, dP = dO V^T), K^T (A of dQ^T = K^T dS^T)
     f32x16 dkacc[NB], dvacc[NB];
     int pend_ctr = -1;  // block whose counter this wave still has to advance
-    int poll_v = -1;    // counter value of the coming block, loaded one step early
+    // The coming block's counter is copied into sm.poll[w] one step early.
+    // vm_poll counts this wave's vector memory operations issued since that
+    // copy (a lower bound is safe: the wait before reading it only gets
+    // longer), vm_rel those issued since the accumulator stores of the
+    // previous block.
+    int vm_poll = 63, vm_rel = 63;
     bool top_wait = true;  // first block of the chain: wait for this wave's LDS loads at the top
 
     auto step_at = [&](int st) -> unsigned { return __builtin_amdgcn_readfirstlane(sm.steps[st]); };
@@ -255,18 +262,19 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     auto load_part = [&](int pb, int b, int k) {  // part k < QLD of the Q and dO rows
       const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
       const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
-      lds_load16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
-      lds_load16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
+      dma16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
+      dma16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
     };
     auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
-      if (w == 0) lds_load4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + l) * 4);
-      if (w == 1) lds_load4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + l) * 4);
+      if (w == 0) dma4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + l) * 4);
+      if (w == 1) dma4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + l) * 4);
     };
     auto load_block = [&](int pb, int b) {
 #pragma unroll
       for (int k = 0; k < QLD; ++k) load_part(pb, b, k);
       load_ld(pb, b);
     };
+    constexpr int kBlockLoads = 2 * QLD;  // direct loads of one block by waves >= 2 (waves 0, 1: one more)
     // The ordered variants keep dQacc in register order: 64-row block pb is
     // BM*D floats at pb*BM*D; wave w's slice (columns [32w, 32w+32)) is the
     // 2048 floats at w*2048, chunk k (= 4 qb + rb) of lane l at k*256 + 4l
@@ -275,7 +283,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     auto acc_off = [&](int pb, int k) { return (uint32_t)(pb * BM * D + w * BM * 32 + k * 256 + 4 * l) * 4; };
     auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) lds_load16_coherent(racc, &acc_w[k * 256], acc_off(pb, k));
+      for (int k = 0; k < 8; ++k) dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -304,7 +312,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     if (st < nsteps) {
       const int pb0 = step_at(st) & 0xfff;
       load_block(pb0, buf);
-      if (ordered) poll_v = __hip_atomic_load(ctr_head + (size_t)pb0 * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (ordered) dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb0 * kCtrStride * 4);
     }
 
     for (; st < nsteps;) {
@@ -332,6 +340,11 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           ktreg[ks] = as_bf16x8(u32x4{t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16),
                                       t[4] | ((unsigned)t[5] << 16), t[6] | ((unsigned)t[7] << 16)});
         }
+        // wait for the operands here, on this path only: otherwise the
+        // compiler guards their first uses in every step with waits that also
+        // drain the prefetch issued in between
+        vm_wait<0>();
+        vm_poll = vm_rel = 63;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -345,7 +358,10 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
       //      loads at the end of the previous block; only a new chain or V tile
       //      waits here), so after the barrier all of it is visible and the other
       //      buffer is free
-      if (top_wait) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (top_wait) {
+        vm_wait<0>();
+        vm_poll = vm_rel = 63;
+      }
       top_wait = false;
       __syncthreads();
 
@@ -477,11 +493,17 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         if (ks < QLD) load_part(pb_next, buf ^ 1, ks);
         if (ks == 0) load_ld(pb_next, buf ^ 1);
       });
-      // ---- ordering: the counter of this block was loaded at the end of the
+      if (pb_next >= 0) {
+        const int n = kBlockLoads + (w < 2 ? 1 : 0);
+        vm_poll += n;
+        vm_rel += n;
+      }
+      // ---- ordering: the counter of this block was copied at the end of the
       //      previous step; if the turn is ours, fetch the accumulator slice
       //      during the next run so its latency hides behind the MFMAs
       if (ordered && !failed) {
-        const int v0 = __builtin_amdgcn_readfirstlane(poll_v);
+        vm_wait_le(vm_poll);  // the copy has landed (the prefetch need not have)
+        const int v0 = __builtin_amdgcn_readfirstlane(sm.poll[w][0]);
         if (v0 >= NW * rank) {
           have_turn = true;
           __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -494,7 +516,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int p = ks * 8 / KS; p < (ks + 1) * 8 / KS; ++p) {
           softmax_piece(0, p);
-          if (early_acc) lds_load16_coherent(racc, &acc_w[p * 256], acc_off(pb, p));
+          if (early_acc) dma16_coherent(racc, &acc_w[p * 256], acc_off(pb, 0), (uint32_t)p * 1024);
         }
       });
       // run 3: dV/dK of half 0, with softmax of half 1
@@ -510,21 +532,18 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         }
       });
 
-      // deferred release of the previous block: when this step prefetched,
-      // its accumulator stores were followed by the 2*QLD = 8 Q / dO loads of
-      // the prefetch (and possibly more), and vector memory operations complete
-      // in issue order, so at most 8 outstanding means the stores are done;
-      // without a prefetch, wait for everything
+      if (early_acc) vm_rel += 8;
+      // deferred release of the previous block: its accumulator stores were
+      // followed by vm_rel operations (this step's prefetch and accumulator
+      // fetch), and vector memory operations complete in issue order, so at
+      // most vm_rel in flight means the stores are done
       if (pend_ctr >= 0) {
-        if (pb_next >= 0)
-          asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-        else
-          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        vm_wait_le(vm_rel);
         release();
       }
       if constexpr (MODE == kModeNoDq) {
         // dK, dV only: the next block's Q / dO have landed before the barrier
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        vm_wait<0>();
       } else {
         __syncthreads();
 
@@ -581,10 +600,10 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           add = have_turn && rank > 0;
         }
         // this wave's slice (and the next block's Q / dO) have landed
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        // sample the next block's counter now, ahead of the stores below
-        if (ordered && pb_next >= 0)
-          poll_v = __hip_atomic_load(ctr_head + (size_t)pb_next * kCtrStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        vm_wait<0>();
+        vm_poll = vm_rel = 0;
+        // copy the next block's counter now, ahead of the stores below
+        if (ordered && pb_next >= 0) dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb_next * kCtrStride * 4);
         if constexpr (ordered) {
           // ---- add this wave's partial into its slice straight from registers:
           //      the accumulator is stored in this wave's register order, so the
@@ -611,6 +630,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
                 st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
               }
             }
+            vm_poll += last ? (a.dq_accum ? 16 : 8) : 8;
           }
         } else if constexpr (MODE == kModePartials) {
           // ---- partials variant: the partial goes to KV tile j's own buffer, in
@@ -642,11 +662,14 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         }
         if (ordered) {
           if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
+          if (w == 0 && a.witness && rank < a.tc) vm_poll += 1;
           pend_ctr = pb;
           if (!deferred || nst >= nsteps) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            vm_wait<0>();  // the copy of the next counter has landed as well
             release();
+            vm_poll = 63;
           }
+          vm_rel = 0;  // (the witness store, if any, is not counted: the wait only gets longer)
         }
       }
       buf ^= 1;

@@ -49,6 +49,70 @@ __device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t o
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
 }
 
+// The same direct loads issued from inline assembly, so the compiler's
+// wait-count pass does not see them.  The builtins above make it guard every
+// later LDS read that it cannot prove disjoint from the target (it cannot for
+// a double buffer with a run-time index, nor through the transposed-read
+// pointer casts) with a full vmcnt(0), which drains the next block's prefetch
+// and the accumulator fetch in the middle of a step.  With these, the caller
+// owns the ordering: before reading the landed bytes it waits with
+// s_waitcnt vmcnt (vm_wait, vm_wait_le), and a workgroup barrier follows when
+// other waves read them.  m0 (the LDS base of the copy) is saved and restored.
+__device__ inline uint32_t lds_base(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p);
+}
+__device__ inline void dma16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+}
+__device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC1: device-coherent
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+}
+// ... with a wave-uniform byte offset added in the scalar offset field, so a
+// run of copies at fixed strides shares one per-lane offset register
+__device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off, uint32_t soff) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc1 lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r), "s"(soff) : "memory");
+}
+__device__ inline void dma4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+}
+__device__ inline void dma4_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC1: device-coherent
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+}
+// Wait until at most N of this wave's vector memory operations are in flight.
+// A real s_waitcnt (the compiler's wait-count pass sees it and drops waits of
+// its own that it makes redundant), then a compiler memory fence so that no
+// LDS read of landed bytes moves above it.  Encoding (gfx9 family): vmcnt in
+// bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima.
+template <int N>
+__device__ inline void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+  asm volatile("" ::: "memory");
+}
+// Wait until at most n (wave-uniform, any value) are in flight: n is rounded
+// down to a supported count, which only waits longer.  Vector memory
+// operations of a wave complete in issue order, so this guarantees that
+// everything issued before the last n of them has completed.
+__device__ inline void vm_wait_le(int n) {
+  if (n >= 24) vm_wait<24>();
+  else if (n >= 17) vm_wait<17>();
+  else if (n >= 16) vm_wait<16>();
+  else if (n >= 9) vm_wait<9>();
+  else if (n >= 8) vm_wait<8>();
+  else if (n >= 1) vm_wait<1>();
+  else vm_wait<0>();
+}
+
 // One step of a chain, packed for the LDS step table: 64-row block pb (12
 // bits), KV tile j (9), rank in the block's summation order (10), last (1).
 // kNoStep marks a step whose block or KV tile lies past N.

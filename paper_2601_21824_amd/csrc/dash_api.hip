@@ -111,7 +111,7 @@ int check_shape(int B, int H, int N, int d) {
 int resolve(int schedule, int d, int causal) {
   switch (schedule) {
     case DASH_SCHED_AUTO:
-      return !causal ? DASH_SCHED_SHIFT : (d <= 128 ? DASH_SCHED_SYMSHIFT : DASH_SCHED_DESCENDING);
+      return causal ? DASH_SCHED_DESCENDING : DASH_SCHED_SHIFT;
     case DASH_SCHED_SHIFT:
       return causal ? DASH_SCHED_SYMSHIFT : DASH_SCHED_SHIFT;
     default:

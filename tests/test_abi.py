@@ -67,8 +67,8 @@ def test_argument_errors_without_device():
 
 def test_schedule_resolution():
     assert b.dash_resolve_schedule("auto", 128, False) == b.DASH_SCHED_SHIFT
-    assert b.dash_resolve_schedule("auto", 128, True) == b.DASH_SCHED_SYMSHIFT
-    assert b.dash_resolve_schedule("auto", 64, True) == b.DASH_SCHED_SYMSHIFT
+    assert b.dash_resolve_schedule("auto", 128, True) == b.DASH_SCHED_DESCENDING
+    assert b.dash_resolve_schedule("auto", 64, True) == b.DASH_SCHED_DESCENDING
     assert b.dash_resolve_schedule("auto", 256, True) == b.DASH_SCHED_DESCENDING
     assert b.dash_resolve_schedule("auto", 256, False) == b.DASH_SCHED_SHIFT
     assert b.dash_resolve_schedule("shift", 64, True) == b.DASH_SCHED_SYMSHIFT
