@@ -23,6 +23,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "bwd_common.h"
+#include "lds_layout.h"
 
 namespace dash {
 
@@ -150,33 +151,14 @@ __global__ __launch_bounds__(256) void bwd_sum_partials_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------- bwd_main
-// LDS tiles of bf16 rows are stored in 16-byte chunks with chunk c of row r at
-// c ^ sw16(r): 8 consecutive rows read at the same chunk (MFMA row operands)
-// and 4 consecutive rows read by ds_read_b64_tr_b16 (transposed operands)
-// both hit 32 distinct banks.  The fp32 dQ staging tile uses c ^ (r & 7).
-__device__ inline int sw16(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
-
-template <int D>
-__device__ inline int bf_at(int r, int col) {  // element index in a [rows][D] bf16 tile
-  return r * D + (((col >> 3) ^ sw16(r)) << 3) + (col & 7);
-}
-template <int D>
-__device__ inline int f_at(int r, int col) {  // element index in a [rows][D] fp32 tile (col % 4 == 0)
-  return r * D + (((col >> 2) ^ (r & 7)) << 2);
-}
-
-// dS^T tile [kv][64 q] bf16: 8-byte slot s of row r lives at s ^ swt(r), so
-// 16-lane 8-byte writes down a column and transposed reads of 4 rows are both
-// bank-conflict free.
-__device__ inline int swt(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-__device__ inline int dst_at(int r, int q) { return r * kBlockRows + (((q >> 2) ^ swt(r)) << 2); }
+// LDS layouts of the Q / dO blocks and the dS^T tile: lds_layout.h.
 
 template <int D>
 struct MainSmem {
   static constexpr int BM = kBlockRows;
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
-  __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], 8-byte slot s of row r at s ^ swt(r)
+  __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], swizzled 8-byte slots (dst_at)
   float acc[BM * D];       // dQ accumulator block: wave w's columns [32w, 32w+32) as [q][8 chunks], chunk c at c ^ (q & 7)
   float ls[2][BM];         // L * log2(e) per query row
   float ds[2][BM];         // D per query row
@@ -260,14 +242,14 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     };
     // Q / dO / L / D of block pb into LDS buffer b (asynchronous, vmcnt)
     auto load_part = [&](int pb, int b, int k) {  // part k < QLD of the Q and dO rows
-      const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ sw16(r);
+      const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ tile_swz<D>(r);
       const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
       dma16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
       dma16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
     };
     auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
-      if (w == 0) dma4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + l) * 4);
-      if (w == 1) dma4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + l) * 4);
+      if (w == 0) dma4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + fresh_lane()) * 4);
+      if (w == 1) dma4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + fresh_lane()) * 4);
     };
     auto load_block = [&](int pb, int b) {
 #pragma unroll
@@ -644,20 +626,25 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         } else {
           // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
           //      atomic per element, each instruction covering two whole 128-byte
-          //      row segments of the row-major dQacc
+          //      row segments of the row-major dQacc.  Staging: 16-byte chunk
+          //      c of row q at c ^ ((q >> 1) & 7), conflict-free for the chunk
+          //      writes (16 rows per lane group) and the row reads (two rows per
+          //      instruction); the read of rows 2k, 2k+1 XORs with k & 7, the
+          //      same for every lane, so no per-row lane offsets stay live.
   #pragma unroll
           for (int k = 0; k < 8; ++k) {
             const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
-            *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ (q & 7))) * 4] =
+            *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ ((q >> 1) & 7))) * 4] =
                 f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
           }
           asm volatile("" ::: "memory");  // lanes read what other lanes wrote
-          const int c = l & 31;
+          const int c = l & 31, hi = l >> 5;
+          const int lane_off = hi * D + 32 * w + c;  // this lane's element of a two-row pair
   #pragma unroll 8
           for (int k = 0; k < 32; ++k) {
-            const int q = 2 * k + (l >> 5);
-            const float v = acc_w[(q * 8 + ((c >> 2) ^ (q & 7))) * 4 + (c & 3)];
-            if (q0 + q < N) atomicAdd(a.dqacc + head + (size_t)(q0 + q) * D + 32 * w + c, v);
+            const float v = acc_w[(2 * k + hi) * 32 + (((c >> 2) ^ (k & 7)) << 2) + (c & 3)];
+            float* rows = a.dqacc + head + (size_t)(q0 + 2 * k) * D;  // wave-uniform
+            if (q0 + 2 * k + hi < N) atomicAdd(rows + lane_off, v);
           }
         }
         if (ordered) {

@@ -25,6 +25,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "bwd_common.h"
+#include "lds_layout.h"
 
 namespace dash {
 namespace {
@@ -43,18 +44,7 @@ __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// [rows][256] bf16 tile: 16-byte chunk c of row r at c ^ s(r).  16 rows read
-// at one chunk (MFMA row operands) and 4 rows x 2 chunks read transposed both
-// fall on distinct banks.
-__device__ inline int qsw(int r) { return ((r & 3) << 1) | ((r >> 2) & 1) | (((r >> 3) & 1) << 3); }
-__device__ inline int q_at(int r, int col) { return r * D + (((col >> 3) ^ qsw(r)) << 3) + (col & 7); }
-// dS^T [64 kv][64 q] bf16: 8-byte slot s (4 queries) of row r at s ^ h(r), for
-// conflict-free 8-byte column writes and 4-row transposed reads.
-__device__ inline int dsw(int r) {
-  const int m = (r >> 1) & 7;
-  return 2 * (((m & 1) << 2) | (m >> 1));
-}
-__device__ inline int ds_at(int r, int q) { return r * BM + (((q >> 2) ^ dsw(r)) << 2) + (q & 3); }
+// LDS layouts of the Q / dO blocks and the dS^T tile: lds_layout.h.
 
 struct Smem256 {
   __bf16 qs[BM * D];     // Q block [q][d]
@@ -128,7 +118,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
       const int t0 = 64 * w + (int)lane;
 #pragma unroll
       for (int k = 0; k < QLD; ++k) {
-        const int slot = k * NT + t0, r = slot / CPR, c = (slot % CPR) ^ qsw(r);
+        const int slot = k * NT + t0, r = slot / CPR, c = (slot % CPR) ^ q256_swz(r);
         const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
         lds_load16(rq, &sm.qs[(k * NT + 64 * w) * 8], off);
         lds_load16(rdo, &sm.dos[(k * NT + 64 * w) * 8], off);
@@ -229,7 +219,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
         auto rd = [&](int ks, bf16x8* op) {
 #pragma unroll
           for (int qb = 0; qb < 4; ++qb) {
-            const int at = q_at(16 * qb + lr, 32 * ks + 8 * gq);
+            const int at = q256_at(16 * qb + lr, 32 * ks + 8 * gq);
             op[qb] = *(const bf16x8*)&sm.qs[at];
             op[4 + qb] = *(const bf16x8*)&sm.dos[at];
           }
@@ -292,7 +282,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
       // dS^T -> LDS: row = key, 4 queries per 8-byte write
 #pragma unroll
       for (int qb = 0; qb < 4; ++qb)
-        *(u32x2*)&sm.dst[ds_at(kvl, 16 * qb + 4 * gq)] =
+        *(u32x2*)&sm.dst[ds256_at(kvl, 16 * qb + 4 * gq)] =
             u32x2{pack_bf16(dp[qb][0], dp[qb][1]), pack_bf16(dp[qb][2], dp[qb][3])};
 
       // ---- dV += P^T dO, dK += dS^T Q: B operand of d block db, k-step kq =
@@ -302,8 +292,8 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
           const int db = k >> 1, kq = k & 1;
           const int col = 16 * db + 4 * (lr & 3);
           const int row = 32 * kq + 4 * gq + (lr >> 2);
-          *bo = as_bf16x8(tr_read(&sm.dos[q_at(row, col)]), tr_read(&sm.dos[q_at(row + 16, col)]));
-          *bqv = as_bf16x8(tr_read(&sm.qs[q_at(row, col)]), tr_read(&sm.qs[q_at(row + 16, col)]));
+          *bo = as_bf16x8(tr_read(&sm.dos[q256_at(row, col)]), tr_read(&sm.dos[q256_at(row + 16, col)]));
+          *bqv = as_bf16x8(tr_read(&sm.qs[q256_at(row, col)]), tr_read(&sm.qs[q256_at(row + 16, col)]));
         };
         constexpr int NP = 2 * NDB, RING = 3;
         bf16x8 ro[RING], rqv[RING];
@@ -341,7 +331,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
         for (int qb = 0; qb < 4; ++qb) {
           const int row = 32 * kk + 8 * gq + (lr >> 2);
           const int col = 16 * qb + 4 * (lr & 3);
-          bds[qb] = as_bf16x8(tr_read(&sm.dst[ds_at(row, col)]), tr_read(&sm.dst[ds_at(row + 4, col)]));
+          bds[qb] = as_bf16x8(tr_read(&sm.dst[ds256_at(row, col)]), tr_read(&sm.dst[ds256_at(row + 4, col)]));
         }
 #pragma unroll
         for (int db = 0; db < 4; ++db)

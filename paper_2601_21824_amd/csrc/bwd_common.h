@@ -88,6 +88,16 @@ __device__ inline void dma4_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
 }
+// The lane index, read afresh where it is called.  Per-lane offsets derived
+// from it are rebuilt in a step instead of being hoisted out of the loop and
+// spilled: a spill reload waits for every vector memory operation in flight,
+// including the copies, stores and atomics the wave has just issued.
+__device__ inline int fresh_lane() {
+  unsigned lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  return (int)lane;
+}
+
 // Wait until at most N of this wave's vector memory operations are in flight.
 // A real s_waitcnt (the compiler's wait-count pass sees it and drops waits of
 // its own that it makes redundant), then a compiler memory fence so that no
