@@ -116,7 +116,20 @@ typedef struct {
      atomic run with any count.  The summation order -- hence every output
      bit -- does not depend on it. */
   int max_workgroups;
+  /* Order in which the persistent workgroups take (head, chain) work items:
+     DASH_TICKETS_AUTO (0, the measured faster order for the schedule and d),
+     DASH_TICKETS_HEAD_MAJOR (1: all chains of a head in a row) or
+     DASH_TICKETS_CHAIN_MAJOR (2: chain w of every head before chain w+1, i.e.
+     the longest chains first under a causal mask; naive, Descending, atomic
+     and the comparison variants only -- Shift and Symmetric Shift need the
+     chains of a head together: DASH_ERR_INVALID_ARG).  The summation order --
+     hence every output bit -- does not depend on it. */
+  int ticket_order;
 } dash_bwd_options_t;
+
+#define DASH_TICKETS_AUTO 0
+#define DASH_TICKETS_HEAD_MAJOR 1
+#define DASH_TICKETS_CHAIN_MAJOR 2
 
 /*
  * Forward attention producing O and L (Algorithm 1's inputs): O = softmax(s QK^T

@@ -23,6 +23,7 @@ SCHEDULES = {"atomic": 0, "naive": 1, "descending": 2, "shift": 3, "symshift": 4
 DASH_OK, DASH_ERR_INVALID_ARG, DASH_ERR_UNSUPPORTED = 0, -1, -2
 DASH_ERR_HIP, DASH_ERR_TIMEOUT, DASH_ERR_NO_DEVICE = -3, -4, -5
 DASH_FLAG_POISON_COUNTERS = 1
+DASH_TICKETS_AUTO, DASH_TICKETS_HEAD_MAJOR, DASH_TICKETS_CHAIN_MAJOR = 0, 1, 2
 
 # every symbol include/dash.h declares
 EXPORTS = ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_bwd_workspace_size",
@@ -40,7 +41,8 @@ class dash_bwd_options_t(ctypes.Structure):
     _fields_ = [("spin_limit", ctypes.c_int), ("flags", ctypes.c_int),
                 ("witness", ctypes.c_void_p), ("partials", ctypes.c_void_p),
                 ("dq_accum", ctypes.c_void_p), ("event_main_begin", ctypes.c_void_p),
-                ("event_main_end", ctypes.c_void_p), ("max_workgroups", ctypes.c_int)]
+                ("event_main_end", ctypes.c_void_p), ("max_workgroups", ctypes.c_int),
+                ("ticket_order", ctypes.c_int)]
 
 
 _lib = None

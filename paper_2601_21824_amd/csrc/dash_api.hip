@@ -195,13 +195,33 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   if (((uintptr_t)workspace & 255) != 0) return fail(DASH_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
   if (opts && opts->spin_limit < 0) return fail(DASH_ERR_INVALID_ARG, "spin_limit must be >= 0");
   if (opts && opts->max_workgroups < 0) return fail(DASH_ERR_INVALID_ARG, "max_workgroups must be >= 0");
+  const int tickets = opts ? opts->ticket_order : DASH_TICKETS_AUTO;
+  if (tickets < DASH_TICKETS_AUTO || tickets > DASH_TICKETS_CHAIN_MAJOR)
+    return fail(DASH_ERR_INVALID_ARG, "unknown ticket_order");
   DeviceInfo di;
   if ((rc = device_info(&di))) return rc;
 
   const int sched = resolve(schedule, d, causal);
-  const dash::Geom G = dash::make_geom(sched, causal, N, d);
+  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
+    return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
   const int occ = d == 64 ? di.occ64 : d == 128 ? di.occ128 : di.occ256;
   const long resident = (long)occ * di.cus;
+  if (tickets != DASH_TICKETS_AUTO) {
+    G.chain_major = tickets == DASH_TICKETS_CHAIN_MAJOR;
+  } else if (sched != DASH_SCHED_SHIFT && sched != DASH_SCHED_SYMSHIFT) {
+    // Chain-major while a head has fewer chains than resident workgroups:
+    // head-major would put all of a head's chains on the GPU at once, and
+    // with naive / Descending every one of them waits out the whole pipeline
+    // fill of the head (chain j's first turn comes j steps late); chain-major
+    // keeps few chains per head in flight and starts the longest first.  The
+    // variants without ordering waits only gain the longest-first balance, so
+    // they go chain-major under a causal mask only.  Once one head's chains
+    // fill the GPU, head-major keeps the resident workgroups on one head's
+    // Q / dO and wins.  (Measured over d = 64 / 128 / 256 and both masks.)
+    const bool waits = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING;
+    G.chain_major = (long)G.chains < resident && (waits || causal);
+  }
   // Shift-type chains wait on each other in a cycle: every chain of a Shift
   // group (Symmetric Shift: of a head) must be able to run at once.  Naive and
   // Descending chains only wait on chains with lower work tickets, which the

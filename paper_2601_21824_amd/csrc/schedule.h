@@ -59,6 +59,7 @@ struct Geom {
   int nsub;    // physical 64-row blocks per scheduling Q tile (= br / 64)
   int chains;  // workgroup chains per head
   int grp;     // SHIFT: chains per group (others: = chains)
+  int chain_major;  // work tickets chain-major (see ticket_chain), else head-major
 };
 
 // rows per KV tile for head dim d
@@ -77,6 +78,7 @@ DASH_HD Geom make_geom(int sched, int causal, int N, int d) {
   G.nsub = G.br / kBlockRows;
   G.chains = sched == S_SYMSHIFT ? G.t_c / 2 : G.t_c;
   G.grp = (sched == S_SHIFT && G.chains > kMaxGroup) ? kMaxGroup : G.chains;
+  G.chain_major = 0;  // the library picks the ticket order per call (device-dependent)
   return G;
 }
 
@@ -137,14 +139,14 @@ DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
   }
 }
 
-// Work ticket -> (head, chain).  Head-major by default (all chains of a head
-// in a row, as Shift and Symmetric Shift need them together).  With a causal
-// mask, the schedules whose waits only point to lower KV tiles go chain-major
-// instead: chain w of every head before chain w+1, i.e. the longest chains
-// first across heads (longest-processing-time order); every chain a wait
-// points to still has a lower ticket.
+// Work ticket -> (head, chain).  Head-major (all chains of a head in a row,
+// as Shift and Symmetric Shift need them together) or, for the schedules whose
+// waits only point to lower KV tiles, chain-major (G.chain_major): chain w of
+// every head before chain w+1, i.e. the longest chains first across heads
+// under a causal mask (longest-processing-time order).  Either way every chain
+// a wait points to has a lower ticket.
 DASH_HD void ticket_chain(const Geom& G, int heads, int item, int* bh, int* w) {
-  if (G.causal && G.sched != S_SYMSHIFT && G.sched != S_SHIFT) {
+  if (G.chain_major) {
     *w = item / heads;
     *bh = item % heads;
   } else {

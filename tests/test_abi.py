@@ -63,6 +63,11 @@ def test_argument_errors_without_device():
     rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
                               16, ctypes.byref(opts), None)
     assert rc == b.DASH_ERR_INVALID_ARG
+    # an unknown ticket order is an argument error (checked before any device call)
+    opts = b.dash_bwd_options_t(0, 0, None, None, None, None, None, 0, 3)
+    rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
+                              1 << 40, ctypes.byref(opts), None)
+    assert rc == b.DASH_ERR_INVALID_ARG and "ticket_order" in b.dash_last_error()
 
 
 def test_schedule_resolution():

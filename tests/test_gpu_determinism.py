@@ -192,6 +192,44 @@ def test_grid_size_does_not_change_bits(case):
         assert e.value.code == dash.DASH_ERR_INVALID_ARG
 
 
+TICKET_CASES = [
+    (2, 4, 2048, 128, True, "naive"),
+    (2, 4, 2048, 128, True, "descending"),
+    (2, 4, 2048, 128, False, "naive"),
+    (1, 4, 4096, 256, True, "descending"),
+    (1, 4, 4096, 256, True, "naive"),
+    (4, 8, 1024, 64, True, "descending"),
+    (2, 4, 2048, 128, True, "split"),
+    (2, 4, 2048, 128, True, "partials"),
+]
+
+
+@pytest.mark.parametrize("case", TICKET_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in TICKET_CASES])
+def test_ticket_order_does_not_change_bits(case):
+    """Head-major and chain-major work tickets (with the GPU's resident grid
+    and with three workgroups) give the same bits as the default order; Shift
+    and Symmetric Shift refuse chain-major tickets."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[tickets] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=19)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d, sched)
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
+    for order in (dash.DASH_TICKETS_HEAD_MAJOR, dash.DASH_TICKETS_CHAIN_MAJOR):
+        for cap in (0, 3):
+            opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap, order)
+            got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts, workspace=ws)
+            assert dash.dash_bwd_check(ws) == dash.DASH_OK
+            for a, b in zip(ref, got):
+                assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"order {order} grid {cap} differs"
+    for s in ("shift", "symshift") if causal else ("shift",):
+        with pytest.raises(dash.DashError) as e:
+            run_bwd(qg, kg, vg, og, dog, lseg, causal, s, workspace=dash.new_workspace(B, H, N, d, s),
+                    options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 0,
+                                                    dash.DASH_TICKETS_CHAIN_MAJOR))
+        assert e.value.code == dash.DASH_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("d", [64, 256])
 def test_shift_groups_order_and_minimal_grid(d):
     """N = 32768 gives 512 KV tiles per head at d = 64 and d = 256 (64-row KV
