@@ -93,7 +93,7 @@ typedef struct {
   /* DASH_FLAG_* bits */
   int flags;
   /* If non-NULL: int32 [B*H][ceil(N/64)][T_c], T_c = ceil(N/bc) KV tiles of
-     bc rows (bc = d for d <= 128, 64 for d = 256; geometry[4] of
+     bc rows (bc = 128 for d <= 128, 64 for d = 256; geometry[4] of
      dash_schedule_table).  The workgroup that adds its partial to 64-row dQ
      block p with order position r writes its KV-tile index at [bh][p][r]
      (ordering witness). */
@@ -183,7 +183,7 @@ int dash_resolve_schedule(int schedule, int d, int causal);
 /*
  * Host-side view of the schedule the kernels follow (no GPU needed).  For one
  * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c
- * KV tiles of bc rows (bc = d for d <= 128, 64 for d = 256).  Writes, when the
+ * KV tiles of bc rows (bc = 128 for d <= 128, 64 for d = 256).  Writes, when the
  * pointer is non-NULL:
  *   geometry[6]            = {T_r, T_c, br, number of workgroup chains per
  *                             head, bc, chains per Shift group (the chains

@@ -3,9 +3,10 @@
 // bwd_pre  : D = rowsum(dO o O) per query row in fp32 (Algorithm 1, the
 //            preprocessing kernel); resets the ordering counters, the work
 //            ticket and the error flag (and dQacc for the atomic variant).
-// bwd_main : one KV tile of d rows per work item, d/32 waves; wave w owns KV
-//            rows [32w, 32w+32) of the tile and keeps K, V, K^T operands and the
-//            dK, dV accumulators in registers for the whole chain.  For every
+// bwd_main : one KV tile of 128 rows per work item (d = 64 and 128), 4 waves;
+//            wave w owns KV rows [32w, 32w+32) of the tile and keeps K, V, K^T
+//            operands and the dK, dV accumulators in registers for the whole
+//            chain.  For every
 //            64-row Q block of the chain (Algorithm 1, the consumer loop):
 //              S = Q K^T, dP = dO V^T            (bf16 MFMA 32x32x16)
 //              P = exp(S - L), dS = P o (dP - D)  (fp32)
@@ -134,10 +135,11 @@ __global__ __launch_bounds__(256) void bwd_sum_partials_kernel(BwdArgs a) {
     const int e4 = (int)(idx % PER);
     const long bp = idx / PER;
     const int pb = (int)(bp % a.nblk), bh = (int)(bp / a.nblk);
-    // register order: slice w (2048 floats), chunk k (256), lane l (4)
-    const int w = e4 >> 9, k = (e4 >> 6) & 7, l = e4 & 63;
-    const int q = pb * BM + 32 * (k >> 2) + (l & 31);
-    const int col = 32 * w + 8 * (k & 3) + 4 * (l >> 5);
+    // register order: 32 x 32 tile T = 2 * (d block) + (query half) of 1024
+    // floats, 1 KB chunk rb of 256 floats, lane l of 4 floats
+    const int T = e4 >> 8, rb = (e4 >> 6) & 3, l = e4 & 63;
+    const int q = pb * BM + 32 * (T & 1) + (l & 31);
+    const int col = 32 * (T >> 1) + 8 * rb + 4 * (l >> 5);
     if (q >= a.n) continue;
     const int c = contributors(a.G, pb / a.G.nsub);
     const f32x4* p = (const f32x4*)(a.dqacc + ((size_t)bh * a.tc * a.nblk + pb) * BM * D) + e4;
@@ -158,30 +160,32 @@ struct MainSmem {
   static constexpr int BM = kBlockRows;
   __bf16 qs[2][BM * D];    // Q block [q][d], double-buffered
   __bf16 dos[2][BM * D];   // dO block [q][d], double-buffered
-  __bf16 dst[D * BM];      // dS^T (bf16) [kv][q], swizzled 8-byte slots (dst_at)
-  float acc[BM * D];       // dQ accumulator block: wave w's columns [32w, 32w+32) as [q][8 chunks], chunk c at c ^ (q & 7)
+  __bf16 dst[kTileKV * BM];  // dS^T (bf16) [kv][q], swizzled 8-byte slots (dst_at)
+  float acc[BM * D];       // dQ accumulator block as it arrives, per-wave slices in register order
   float ls[2][BM];         // L * log2(e) per query row
   float ds[2][BM];         // D per query row
   unsigned steps[kMaxChainSteps];  // this chain's blocks, see pack_step
-  int poll[D / 32][64];  // per wave: the coming block's counter (direct load, all lanes alike)
+  int poll[kTileKV / 32][64];  // per wave: the coming block's counter (direct load, all lanes alike)
   int item;
 };
 
 template <int D, bool CAUSAL, int MODE>
-__global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
-  constexpr int NW = D / 32;    // waves
+__global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
+  constexpr int BC = kTileKV;   // KV rows per tile (128 for d = 64 and 128)
+  constexpr int NW = BC / 32;   // waves, 32 KV rows each
   constexpr int NT = 64 * NW;   // threads
-  constexpr int BC = D;         // KV rows per tile
   constexpr int BM = kBlockRows;
   constexpr int KS = D / 16;    // k-steps over d
   constexpr int KSC = BC / 16;  // k-steps over kv
   constexpr int NB = D / 32;    // 32-column blocks of d
   constexpr int CPR = D / 8;    // 16-byte bf16 chunks per row
-  constexpr int FCR = D / 4;    // 16-byte fp32 chunks per row
   constexpr int QLD = BM * CPR / NT;   // direct loads per thread for a Q / dO block
-  constexpr int KLD = BC * CPR / NT;   // ... for the K tile
-  constexpr int ALD = BM * FCR / NT;   // ... for the accumulator block
-  static_assert(NT == 2 * D && QLD == 4 && ALD == 8, "thread/tile shape");
+  // dQ^T of a block is (D / 32) x 2 tiles of 32 x 32 (d block, query half),
+  // tile T = 2 * (d block) + (query half); wave w computes tiles
+  // [w * DQT, (w + 1) * DQT): one d block and one or both query halves
+  constexpr int DQT = D / 64;
+  constexpr int NACC = 4 * DQT;  // its accumulator slice in 1 KB chunks
+  static_assert(NT == 256 && QLD * 32 == D && BM * D == NW * DQT * 1024, "thread/tile shape");
   __shared__ __attribute__((aligned(16))) MainSmem<D> sm;
 
   const Geom G = a.G;
@@ -189,6 +193,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
   const int tid = threadIdx.x, l = tid & 63, g = l >> 5, lc = l & 31;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L16 = l & 15, nh = (l >> 4) & 1;  // transpose-read lane roles
+  const int dblk = (w * DQT) >> 1, qh0 = (w * DQT) & 1;  // this wave's d block, first query half
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   const int total = a.bh * G.chains;
@@ -258,14 +263,15 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
     };
     constexpr int kBlockLoads = 2 * QLD;  // direct loads of one block by waves >= 2 (waves 0, 1: one more)
     // The ordered variants keep dQacc in register order: 64-row block pb is
-    // BM*D floats at pb*BM*D; wave w's slice (columns [32w, 32w+32)) is the
-    // 2048 floats at w*2048, chunk k (= 4 qb + rb) of lane l at k*256 + 4l
-    // holding row 32qb + l%32, columns 32w + 8rb + 4(l/32) .. +3.
-    float* acc_w = &sm.acc[w * BM * 32];
-    auto acc_off = [&](int pb, int k) { return (uint32_t)(pb * BM * D + w * BM * 32 + k * 256 + 4 * l) * 4; };
+    // BM*D floats at pb*BM*D, 32 x 32 tile T at T*1024; wave w's slice (its
+    // DQT tiles) is at w*DQT*1024, and its chunk k (tile w*DQT + k/4, rb = k%4)
+    // of lane l at k*256 + 4l holds row 32 (qh0 + k/4) + l%32, columns
+    // 32 dblk + 8rb + 4(l/32) .. +3.
+    float* acc_w = &sm.acc[w * DQT * 1024];
+    auto acc_off = [&](int pb, int k) { return (uint32_t)(pb * BM * D + w * DQT * 1024 + k * 256 + 4 * l) * 4; };
     auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
+      for (int k = 0; k < NACC; ++k) dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -313,12 +319,12 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           kreg[ks] = as_bf16x8(ld16(rk, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
           vreg[ks] = as_bf16x8(ld16(rv, (uint32_t)(kvr * D + 16 * ks + 8 * g) * 2));
         }
-        // K^T operand: lane holds column d = 32w + lc of K over keys 16ks + 8g .. +7
+        // K^T operand: lane holds column d = 32 dblk + lc of K over keys 16ks + 8g .. +7
 #pragma unroll
         for (int ks = 0; ks < KSC; ++ks) {
           unsigned short t[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t[e] = ld2(rk, (uint32_t)((kv0 + 16 * ks + 8 * g + e) * D + 32 * w + lc) * 2);
+          for (int e = 0; e < 8; ++e) t[e] = ld2(rk, (uint32_t)((kv0 + 16 * ks + 8 * g + e) * D + 32 * dblk + lc) * 2);
           ktreg[ks] = as_bf16x8(u32x4{t[0] | ((unsigned)t[1] << 16), t[2] | ((unsigned)t[3] << 16),
                                       t[4] | ((unsigned)t[5] << 16), t[6] | ((unsigned)t[7] << 16)});
         }
@@ -498,7 +504,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int p = ks * 8 / KS; p < (ks + 1) * 8 / KS; ++p) {
           softmax_piece(0, p);
-          if (early_acc) dma16_coherent(racc, &acc_w[p * 256], acc_off(pb, 0), (uint32_t)p * 1024);
+          if (early_acc && p < NACC) dma16_coherent(racc, &acc_w[p * 256], acc_off(pb, 0), (uint32_t)p * 1024);
         }
       });
       // run 3: dV/dK of half 0, with softmax of half 1
@@ -514,7 +520,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
         }
       });
 
-      if (early_acc) vm_rel += 8;
+      if (early_acc) vm_rel += NACC;
       // deferred release of the previous block: its accumulator stores were
       // followed by vm_rel operations (this step's prefetch and accumulator
       // fetch), and vector memory operations complete in issue order, so at
@@ -531,41 +537,43 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 
         // ---- dQ^T_loc (rows d in [32w, 32w+32), all 64 queries) = K^T dS^T,
         //      k-step ks reads A = K^T (shared by both query halves) and two B's
-        f32x16 dq[2];
+        f32x16 dq[DQT];
   #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int t = 0; t < DQT; ++t)
   #pragma unroll
-          for (int r = 0; r < 16; ++r) dq[qb][r] = 0.f;
+          for (int r = 0; r < 16; ++r) dq[t][r] = 0.f;
         {
           constexpr int RING = 3;
-          auto rd = [&](int ks, bf16x8* b0, bf16x8* b1) {
+          auto rd = [&](int ks, bf16x8* bt) {
             const int krow = 16 * ks + 8 * g + (L16 >> 2);
-            const int qc0 = 16 * nh + 4 * (L16 & 3), qc1 = 32 + qc0;
-            *b0 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc0)]), tr_read(&sm.dst[dst_at(krow + 4, qc0)]));
-            *b1 = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc1)]), tr_read(&sm.dst[dst_at(krow + 4, qc1)]));
-          };
-          bf16x8 rb0[RING], rb1[RING];
   #pragma unroll
-          for (int k = 0; k < RING; ++k) rd(k, &rb0[k], &rb1[k]);
+            for (int t = 0; t < DQT; ++t) {
+              const int qc = 32 * (qh0 + t) + 16 * nh + 4 * (L16 & 3);
+              bt[t] = as_bf16x8(tr_read(&sm.dst[dst_at(krow, qc)]), tr_read(&sm.dst[dst_at(krow + 4, qc)]));
+            }
+          };
+          bf16x8 rb[RING][DQT];
+  #pragma unroll
+          for (int k = 0; k < RING; ++k) rd(k, rb[k]);
   #pragma unroll
           for (int ks = 0; ks < KSC; ++ks) {
             __builtin_amdgcn_sched_barrier(0);
-            dq[0] = mfma32(ktreg[ks], rb0[ks % RING], dq[0]);
-            dq[1] = mfma32(ktreg[ks], rb1[ks % RING], dq[1]);
-            if (ks + RING < KSC) rd(ks + RING, &rb0[ks % RING], &rb1[ks % RING]);
+  #pragma unroll
+            for (int t = 0; t < DQT; ++t) dq[t] = mfma32(ktreg[ks], rb[ks % RING][t], dq[t]);
+            if (ks + RING < KSC) rd(ks + RING, rb[ks % RING]);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-        // dq[qb][r] <-> query 32qb + lc, column d = 32w + 8(r/4) + 4g + r%4
+        // dq[t][r] <-> query 32 (qh0 + t) + lc, column d = 32 dblk + 8(r/4) + 4g + r%4
 
         if (a.partials) {
           const auto rp = make_rsrc(a.partials + ((size_t)bh * a.tc + j) * N * D, hbytes * 2);
   #pragma unroll
-          for (int qb = 0; qb < 2; ++qb)
+          for (int t = 0; t < DQT; ++t)
   #pragma unroll
             for (int rb = 0; rb < 4; ++rb)
-              st16(rp, (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g) * 4,
-                   __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+              st16(rp, (uint32_t)((q0 + 32 * (qh0 + t) + lc) * D + 32 * dblk + 8 * rb + 4 * g) * 4,
+                   __builtin_bit_cast(u32x4, f32x4{dq[t][4 * rb], dq[t][4 * rb + 1], dq[t][4 * rb + 2], dq[t][4 * rb + 3]}));
         }
 
         bool add = false;  // accumulate into the slice (else: the partial is stored as is)
@@ -594,34 +602,34 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           //      schedule's.
           if (have_turn) {
             const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
-            f32x4 old[8];
+            f32x4 old[NACC];
   #pragma unroll
-            for (int k = 0; k < 8; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+            for (int k = 0; k < NACC; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
   #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-              const int qb = k >> 2, rb = k & 3;
-              f32x4 v = {dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+            for (int k = 0; k < NACC; ++k) {
+              const int t = k >> 2, rb = k & 3;
+              f32x4 v = {dq[t][4 * rb], dq[t][4 * rb + 1], dq[t][4 * rb + 2], dq[t][4 * rb + 3]};
               const f32x4 sum = old[k] + v;
   #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
               if (last) {
-                const uint32_t off = (uint32_t)((q0 + 32 * qb + lc) * D + 32 * w + 8 * rb + 4 * g);
+                const uint32_t off = (uint32_t)((q0 + 32 * (qh0 + t) + lc) * D + 32 * dblk + 8 * rb + 4 * g);
                 st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
                 if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
               } else {
                 st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
               }
             }
-            vm_poll += last ? (a.dq_accum ? 16 : 8) : 8;
+            vm_poll += last ? (a.dq_accum ? 2 * NACC : NACC) : NACC;
           }
         } else if constexpr (MODE == kModePartials) {
           // ---- partials variant: the partial goes to KV tile j's own buffer, in
           //      the same register order as the ordered accumulator
           const auto rpb = make_rsrc(a.dqacc + ((size_t)bh * a.tc + j) * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
   #pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const int qb = k >> 2, rb = k & 3;
-            st16(rpb, acc_off(pb, k), __builtin_bit_cast(u32x4, f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]}));
+          for (int k = 0; k < NACC; ++k) {
+            const int t = k >> 2, rb = k & 3;
+            st16(rpb, acc_off(pb, k), __builtin_bit_cast(u32x4, f32x4{dq[t][4 * rb], dq[t][4 * rb + 1], dq[t][4 * rb + 2], dq[t][4 * rb + 3]}));
           }
         } else {
           // ---- atomic variant: partial -> LDS (row-major slice), then one fp32
@@ -631,20 +639,22 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
           //      writes (16 rows per lane group) and the row reads (two rows per
           //      instruction); the read of rows 2k, 2k+1 XORs with k & 7, the
           //      same for every lane, so no per-row lane offsets stay live.
+          //      Staged row rr of the wave's slice is block row 32 qh0 + rr.
   #pragma unroll
-          for (int k = 0; k < 8; ++k) {
-            const int qb = k >> 2, rb = k & 3, q = 32 * qb + lc;
-            *(f32x4*)&acc_w[(q * 8 + ((2 * rb + g) ^ ((q >> 1) & 7))) * 4] =
-                f32x4{dq[qb][4 * rb], dq[qb][4 * rb + 1], dq[qb][4 * rb + 2], dq[qb][4 * rb + 3]};
+          for (int k = 0; k < NACC; ++k) {
+            const int t = k >> 2, rb = k & 3, rr = 32 * t + lc;
+            *(f32x4*)&acc_w[(rr * 8 + ((2 * rb + g) ^ ((rr >> 1) & 7))) * 4] =
+                f32x4{dq[t][4 * rb], dq[t][4 * rb + 1], dq[t][4 * rb + 2], dq[t][4 * rb + 3]};
           }
           asm volatile("" ::: "memory");  // lanes read what other lanes wrote
           const int c = l & 31, hi = l >> 5;
-          const int lane_off = hi * D + 32 * w + c;  // this lane's element of a two-row pair
+          const int lane_off = hi * D + 32 * dblk + c;  // this lane's element of a two-row pair
+          const int qr0 = q0 + 32 * qh0;
   #pragma unroll 8
-          for (int k = 0; k < 32; ++k) {
+          for (int k = 0; k < 16 * DQT; ++k) {
             const float v = acc_w[(2 * k + hi) * 32 + (((c >> 2) ^ (k & 7)) << 2) + (c & 3)];
-            float* rows = a.dqacc + head + (size_t)(q0 + 2 * k) * D;  // wave-uniform
-            if (q0 + 2 * k + hi < N) atomicAdd(rows + lane_off, v);
+            float* rows = a.dqacc + head + (size_t)(qr0 + 2 * k) * D;  // wave-uniform
+            if (qr0 + 2 * k + hi < N) atomicAdd(rows + lane_off, v);
           }
         }
         if (ordered) {
@@ -669,7 +679,7 @@ __global__ __launch_bounds__(2 * D) void bwd_main_kernel(BwdArgs a) {
 
 template <int D, bool CAUSAL>
 void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
-  const dim3 grid(grid_main), block(2 * D);
+  const dim3 grid(grid_main), block(256);
   if (a.G.sched == S_ATOMIC)
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeAtomic>), grid, block, 0, stream, a);
   else if (a.G.sched == S_PARTIALS)
@@ -729,7 +739,7 @@ int main_occupancy() {
                         (const void*)bwd_main_kernel<D, true, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeNoDq>};
   for (const void* f : fns) {
     int blocks = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 2 * D, 0) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 256, 0) != hipSuccess) return 0;
     lo = blocks < lo ? blocks : lo;
   }
   return lo;

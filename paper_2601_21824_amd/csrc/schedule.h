@@ -1,6 +1,6 @@
 // schedule.h -- closed-form dQ-reduction schedules, usable on host and device.
 //
-// One attention head of N rows is cut into KV tiles of BC rows (BC = d for
+// One attention head of N rows is cut into KV tiles of BC rows (BC = 128 for
 // d <= 128, 64 for d = 256: one workgroup's resident K_j, V_j, dK_j, dV_j)
 // and scheduling Q tiles of br rows;
 // a scheduling Q tile is processed as br/64 physical 64-row blocks, each with
@@ -46,12 +46,13 @@ namespace dash {
 enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4, S_PARTIALS = 6, S_SPLIT = 7 };
 
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
+constexpr int kTileKV = 128;    // KV rows per tile of the d = 64 / 128 kernel
 constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident
 
 struct Geom {
   int sched;   // Sched
   int causal;  // 0/1
-  int bc;      // rows per KV tile (= head dim)
+  int bc;      // rows per KV tile (kv_tile_rows)
   int br;      // rows per scheduling Q tile (64, or bc when causal)
   int g;       // bc / br
   int t_c;     // KV tiles per head (SYMSHIFT: rounded up to even)
@@ -63,7 +64,7 @@ struct Geom {
 };
 
 // rows per KV tile for head dim d
-DASH_HD int kv_tile_rows(int d) { return d <= 128 ? d : 64; }
+DASH_HD int kv_tile_rows(int d) { return d <= 128 ? 128 : 64; }
 
 DASH_HD Geom make_geom(int sched, int causal, int N, int d) {
   Geom G;

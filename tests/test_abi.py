@@ -97,9 +97,9 @@ def test_schedule_table_matches_oracle(sched, causal, N, d):
     concrete = b.dash_resolve_schedule(sched, d, causal)
     kind = KINDS[concrete]
     t_r, t_c, br, bc, grp = tab["t_r"], tab["t_c"], tab["br"], tab["bc"], tab["group"]
-    # tile sizes: KV tiles of d rows (64 at d = 256); Q tiles of 64 rows (full)
+    # tile sizes: KV tiles of 128 rows (64 at d = 256); Q tiles of 64 rows (full)
     # or KV-tile rows (causal); Shift groups of at most 256 chains
-    assert bc == (d if d <= 128 else 64)
+    assert bc == (128 if d <= 128 else 64)
     assert br == (bc if causal else 64) and t_r * br == t_c * bc
     assert grp == (min(t_c, 256) if kind == osched.SHIFT else tab["chains"])
     ref = osched.build(kind, t_r, t_c, causal, br, bc, group=grp if kind == osched.SHIFT else None)

@@ -230,13 +230,14 @@ def test_ticket_order_does_not_change_bits(case):
         assert e.value.code == dash.DASH_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("d", [64, 256])
+@pytest.mark.parametrize("d", [256])
 def test_shift_groups_order_and_minimal_grid(d):
-    """N = 32768 gives 512 KV tiles per head at d = 64 and d = 256 (64-row KV
-    tiles), so full-mask Shift runs as two groups of 256 chains: the order the
-    workgroups added their partials in equals the oracle's group-major order,
-    and a grid of exactly one group (256 workgroups) gives the same bits as the
-    default grid."""
+    """N = 32768 gives 512 KV tiles per head at d = 256 (64-row KV tiles), so
+    full-mask Shift runs as two groups of 256 chains: the order the workgroups
+    added their partials in equals the oracle's group-major order, and a grid
+    of exactly one group (256 workgroups) gives the same bits as the default
+    grid.  (With 128-row KV tiles, d = 64 and 128 stay within one group up to
+    N = 32768.)"""
     B, H, N, causal = 1, 1, 32768, False
     print(f"\n[groups] N={N} d={d}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=41, sigma=0.5)
