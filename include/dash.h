@@ -112,9 +112,10 @@ typedef struct {
   /* If > 0: at most this many persistent workgroups for the main kernel (0 =
      as many as the GPU keeps resident).  Shift needs at least the chains of
      one group (geometry[5] of dash_schedule_table), Symmetric Shift the
-     chains of one head, else DASH_ERR_INVALID_ARG; naive, Descending and
-     atomic run with any count.  The summation order -- hence every output
-     bit -- does not depend on it. */
+     chains of one head -- under XCD placement that many per XCD, i.e. times
+     the number of XCDs -- else DASH_ERR_INVALID_ARG; naive, Descending and
+     atomic run with any count (XCD placement: at least one per XCD).  The
+     summation order -- hence every output bit -- does not depend on it. */
   int max_workgroups;
   /* Order in which the persistent workgroups take (head, chain) work items:
      DASH_TICKETS_AUTO (0, the measured faster order for the schedule and d),
@@ -125,11 +126,32 @@ typedef struct {
      chains of a head together: DASH_ERR_INVALID_ARG).  The summation order --
      hence every output bit -- does not depend on it. */
   int ticket_order;
+  /* Where the chains of a head run (see DASH_PLACEMENT_*).  0 = AUTO.  The
+     placement can change Shift's summation order (its group size, geometry[5]
+     of dash_schedule_table) when a head has more than 32 KV tiles; no other
+     schedule's. */
+  int placement;
 } dash_bwd_options_t;
 
 #define DASH_TICKETS_AUTO 0
 #define DASH_TICKETS_HEAD_MAJOR 1
 #define DASH_TICKETS_CHAIN_MAJOR 2
+
+/* Placement of the work of a head.
+   XCD: every chain of head bh runs on XCD (die) bh % n_xcd, whose L2 then
+   holds that head's dQ accumulator and counters -- no other XCD touches them,
+   so the accumulator is read and written through the L2 instead of the
+   device-coherent path.  Each XCD takes work from its own ticket queue; a
+   Shift group is then at most 32 chains (what one XCD keeps resident), and a
+   head's groups run one after another.  Ordered schedules (naive, Descending,
+   Shift, Symmetric Shift) at d = 64 and 128, when the chains that must run at
+   once fit one XCD (Symmetric Shift: T_c <= 64).
+   GLOBAL: one ticket queue for the whole GPU (any schedule, any d).
+   AUTO: XCD when it is possible and B*H is at least the number of XCDs, else
+   GLOBAL (dash_bwd_placement tells which). */
+#define DASH_PLACEMENT_AUTO 0
+#define DASH_PLACEMENT_GLOBAL 1
+#define DASH_PLACEMENT_XCD 2
 
 /*
  * Forward attention producing O and L (Algorithm 1's inputs): O = softmax(s QK^T
@@ -180,11 +202,17 @@ int dash_bwd_check(void* workspace, void* stream);
 /* The concrete schedule DASH_SCHED_AUTO / SHIFT resolve to for (d, causal). */
 int dash_resolve_schedule(int schedule, int d, int causal);
 
+/* The placement (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD) that
+   dash_attn_bwd_ex picks with placement AUTO for this problem on the current
+   device, or a negative dash_status_t.  Needs the device (queries it once). */
+int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule);
+
 /*
  * Host-side view of the schedule the kernels follow (no GPU needed).  For one
  * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c
- * KV tiles of bc rows (bc = 128 for d <= 128, 64 for d = 256).  Writes, when the
- * pointer is non-NULL:
+ * KV tiles of bc rows (bc = 128 for d <= 128, 64 for d = 256), under
+ * `placement` (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD; only Shift's
+ * groups depend on it).  Writes, when the pointer is non-NULL:
  *   geometry[6]            = {T_r, T_c, br, number of workgroup chains per
  *                             head, bc, chains per Shift group (the chains
  *                             that must run at the same time; = chains for
@@ -197,7 +225,7 @@ int dash_resolve_schedule(int schedule, int d, int causal);
  *                            order (-1 when they do not interact)
  * Returns a dash_status_t.
  */
-int dash_schedule_table(int schedule, int N, int d, int causal, int* geometry, int* chain_len,
+int dash_schedule_table(int schedule, int N, int d, int causal, int placement, int* geometry, int* chain_len,
                         int* task_kv, int* task_q, int* rank);
 
 const char* dash_last_error(void);

@@ -24,11 +24,12 @@ DASH_OK, DASH_ERR_INVALID_ARG, DASH_ERR_UNSUPPORTED = 0, -1, -2
 DASH_ERR_HIP, DASH_ERR_TIMEOUT, DASH_ERR_NO_DEVICE = -3, -4, -5
 DASH_FLAG_POISON_COUNTERS = 1
 DASH_TICKETS_AUTO, DASH_TICKETS_HEAD_MAJOR, DASH_TICKETS_CHAIN_MAJOR = 0, 1, 2
+DASH_PLACEMENT_AUTO, DASH_PLACEMENT_GLOBAL, DASH_PLACEMENT_XCD = 0, 1, 2
 
 # every symbol include/dash.h declares
 EXPORTS = ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_bwd_workspace_size",
            "dash_attn_bwd_ex", "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table",
-           "dash_last_error", "dash_release_workspace")
+           "dash_bwd_placement", "dash_last_error", "dash_release_workspace")
 
 
 class DashError(RuntimeError):
@@ -42,7 +43,7 @@ class dash_bwd_options_t(ctypes.Structure):
                 ("witness", ctypes.c_void_p), ("partials", ctypes.c_void_p),
                 ("dq_accum", ctypes.c_void_p), ("event_main_begin", ctypes.c_void_p),
                 ("event_main_end", ctypes.c_void_p), ("max_workgroups", ctypes.c_int),
-                ("ticket_order", ctypes.c_int)]
+                ("ticket_order", ctypes.c_int), ("placement", ctypes.c_int)]
 
 
 _lib = None
@@ -66,11 +67,12 @@ def load():
         lib.dash_bwd_workspace_size.restype = sz
         lib.dash_bwd_check.argtypes = [vp, vp]
         lib.dash_resolve_schedule.argtypes = [ci] * 3
-        lib.dash_schedule_table.argtypes = [ci] * 4 + [ip] * 5
+        lib.dash_schedule_table.argtypes = [ci] * 5 + [ip] * 5
+        lib.dash_bwd_placement.argtypes = [ci] * 6
         lib.dash_last_error.restype = ctypes.c_char_p
         lib.dash_release_workspace.restype = None
         for f in ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_attn_bwd_ex",
-                  "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table"):
+                  "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table", "dash_bwd_placement"):
             getattr(lib, f).restype = ci
         _lib = lib
     return _lib
@@ -168,11 +170,19 @@ def dash_bwd_check(workspace, stream=None) -> int:
     return load().dash_bwd_check(_ptr(workspace), _stream(stream))
 
 
-def dash_schedule_table(schedule, N: int, d: int, causal: bool) -> dict:
-    """The schedule the kernels follow for one head (host computation)."""
+def dash_bwd_placement(B: int, H: int, N: int, d: int, causal: bool, schedule="auto") -> int:
+    """The placement AUTO picks on the current device (DASH_PLACEMENT_GLOBAL / _XCD)."""
+    rc = load().dash_bwd_placement(B, H, N, d, int(causal), _sched(schedule))
+    if rc < 0:
+        _check(rc)
+    return rc
+
+
+def dash_schedule_table(schedule, N: int, d: int, causal: bool, placement=DASH_PLACEMENT_GLOBAL) -> dict:
+    """The schedule the kernels follow for one head under ``placement`` (host computation)."""
     lib = load()
     geo = (ctypes.c_int * 6)()
-    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), geo, None, None, None, None))
+    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), placement, geo, None, None, None, None))
     t_r, t_c, br, chains, bc, grp = list(geo)
     cap = t_r + 1
     chain_len = np.zeros(chains, np.int32)
@@ -180,7 +190,7 @@ def dash_schedule_table(schedule, N: int, d: int, causal: bool) -> dict:
     task_q = np.full(chains * cap, -1, np.int32)
     rank = np.zeros(t_r * t_c, np.int32)
     p = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
-    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), geo, p(chain_len), p(task_kv),
+    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), placement, geo, p(chain_len), p(task_kv),
                                    p(task_q), p(rank)))
     return dict(t_r=t_r, t_c=t_c, br=br, chains=chains, bc=bc, group=grp, chain_len=chain_len,
                 task_kv=task_kv.reshape(chains, cap), task_q=task_q.reshape(chains, cap),

@@ -67,6 +67,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a, int zero_acc) {
     a.ctrl[kCtrlTicket] = 0;
     a.ctrl[kCtrlError] = 0;
   }
+  if (gtid < kMaxXcd) a.ctrl[kCtrlXcdTicket + gtid] = 0;
   // every chain's step table (the same for every head): entry 0 is the number
   // of steps; entry 1 + st is step st, i.e. 64-row block pb of Q tile i with
   // KV tile j, its rank in the block's summation order and whether it is the
@@ -90,13 +91,26 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a, int zero_acc) {
       const int rank = rank_of(G, i, j);
       a.steps[x] = (pb * kBlockRows < a.n && j * bc < a.n) ? pack_step(pb, j, rank, rank == contributors(G, i) - 1) : kNoStep;
     }
-    // work ticket -> (head, chain)
-    const long nitems = (long)a.bh * G.chains;
-    for (long x = gtid; x < nitems; x += nthreads) {
-      int bh, w;
-      ticket_chain(G, a.bh, (int)x, &bh, &w);
-      a.order[2 * x] = bh;
-      a.order[2 * x + 1] = w;
+    // work ticket -> (head, chain); XCD-local placement: one segment of
+    // xcd_cap tickets per XCD
+    if (a.nxcd > 0) {
+      const long nitems = (long)a.nxcd * a.xcd_cap;
+      for (long x = gtid; x < nitems; x += nthreads) {
+        const int q = (int)(x / a.xcd_cap), t = (int)(x % a.xcd_cap);
+        if (t >= xcd_heads(a.bh, a.nxcd, q) * G.chains) continue;
+        int bh, w;
+        ticket_chain_xcd(G, a.bh, a.nxcd, q, t, &bh, &w);
+        a.order[2 * x] = bh;
+        a.order[2 * x + 1] = w;
+      }
+    } else {
+      const long nitems = (long)a.bh * G.chains;
+      for (long x = gtid; x < nitems; x += nthreads) {
+        int bh, w;
+        ticket_chain(G, a.bh, (int)x, &bh, &w);
+        a.order[2 * x] = bh;
+        a.order[2 * x + 1] = w;
+      }
     }
   }
   if (zero_acc) {
@@ -196,8 +210,15 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const int dblk = (w * DQT) >> 1, qh0 = (w * DQT) & 1;  // this wave's d block, first query half
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
-  const int total = a.bh * G.chains;
-  constexpr bool ordered = MODE == kModeOrdered;
+  constexpr bool ordered = MODE == kModeOrdered || MODE == kModeOrderedXcd;
+  // XCD-local placement: this workgroup serves the heads of its own XCD from
+  // that XCD's ticket queue, and the accumulator is read and written through
+  // the XCD's L2 (no other XCD touches those heads)
+  constexpr bool xcd = MODE == kModeOrderedXcd;
+  const int xq = xcd ? xcc_id() : 0;
+  const int total = xcd ? (xq < a.nxcd ? xcd_heads(a.bh, a.nxcd, xq) * G.chains : 0) : a.bh * G.chains;
+  int* const ticket = &a.ctrl[xcd ? kCtrlXcdTicket + xq : kCtrlTicket];
+  const int* const order = a.order + (xcd ? 2 * xq * a.xcd_cap : 0);
   // Shift-type orders are conflict-free: the next contributor to a block reaches
   // it at least one step later, so the counter release can wait until the next
   // step's barrier, by which time the accumulator stores have drained.
@@ -205,14 +226,14 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   bool failed = false;  // this wave hit a wait timeout: skip further waits
 
   for (;;) {
-    if (tid == 0) sm.item = atomicAdd(&a.ctrl[kCtrlTicket], 1);
+    if (tid == 0) sm.item = atomicAdd(ticket, 1);
     __syncthreads();
     const int item = __builtin_amdgcn_readfirstlane(sm.item);  // wave-uniform (SGPR)
     if (item >= total) break;
     // (head, chain) of the ticket from bwd_pre's table; wave-uniform, so the
     // head's buffer descriptors stay in SGPRs
-    const int bh = __builtin_amdgcn_readfirstlane(a.order[2 * item]);
-    const int wch = __builtin_amdgcn_readfirstlane(a.order[2 * item + 1]);
+    const int bh = __builtin_amdgcn_readfirstlane(order[2 * item]);
+    const int wch = __builtin_amdgcn_readfirstlane(order[2 * item + 1]);
     const size_t head = (size_t)bh * N * D;
     const auto rq = make_rsrc((const __bf16*)a.q + head, hbytes);
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
@@ -269,9 +290,17 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     // 32 dblk + 8rb + 4(l/32) .. +3.
     float* acc_w = &sm.acc[w * DQT * 1024];
     auto acc_off = [&](int pb, int k) { return (uint32_t)(pb * BM * D + w * DQT * 1024 + k * 256 + 4 * l) * 4; };
+    // block pb's counter into this wave's poll slot.  The counters stay
+    // device-coherent under XCD-local placement too: the atomic adds are
+    // performed past the L2, so an L2 read of a counter can stay stale.
+    auto poll_copy = [&](int pb) { dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb * kCtrStride * 4); };
+    auto acc_copy = [&](int pb, int k) {  // chunk k of the slice into its landing pad
+      if constexpr (xcd) dma16_l2(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
+      else dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
+    };
     auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int k = 0; k < NACC; ++k) dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
+      for (int k = 0; k < NACC; ++k) acc_copy(pb, k);
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -300,7 +329,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     if (st < nsteps) {
       const int pb0 = step_at(st) & 0xfff;
       load_block(pb0, buf);
-      if (ordered) dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb0 * kCtrStride * 4);
+      if (ordered) poll_copy(pb0);
     }
 
     for (; st < nsteps;) {
@@ -504,7 +533,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int p = ks * 8 / KS; p < (ks + 1) * 8 / KS; ++p) {
           softmax_piece(0, p);
-          if (early_acc && p < NACC) dma16_coherent(racc, &acc_w[p * 256], acc_off(pb, 0), (uint32_t)p * 1024);
+          if (early_acc && p < NACC) acc_copy(pb, p);
         }
       });
       // run 3: dV/dK of half 0, with softmax of half 1
@@ -593,7 +622,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         vm_wait<0>();
         vm_poll = vm_rel = 0;
         // copy the next block's counter now, ahead of the stores below
-        if (ordered && pb_next >= 0) dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb_next * kCtrStride * 4);
+        if (ordered && pb_next >= 0) poll_copy(pb_next);
         if constexpr (ordered) {
           // ---- add this wave's partial into its slice straight from registers:
           //      the accumulator is stored in this wave's register order, so the
@@ -617,7 +646,8 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
                 st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
                 if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
               } else {
-                st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+                if constexpr (xcd) st16(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+                else st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
               }
             }
             vm_poll += last ? (a.dq_accum ? 2 * NACC : NACC) : NACC;
@@ -686,6 +716,8 @@ void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModePartials>), grid, block, 0, stream, a);
   else if (a.G.sched == S_SPLIT)
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeNoDq>), grid, block, 0, stream, a);
+  else if (a.nxcd > 0)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrderedXcd>), grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered>), grid, block, 0, stream, a);
 }
@@ -733,10 +765,12 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 template <int D>
 int main_occupancy() {
   int lo = 1 << 30;
-  const void* fns[8] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
-                        (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, false, kModeNoDq>,
-                        (const void*)bwd_main_kernel<D, true, kModeAtomic>, (const void*)bwd_main_kernel<D, true, kModeOrdered>,
-                        (const void*)bwd_main_kernel<D, true, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeNoDq>};
+  const void* fns[10] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
+                         (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, false, kModeNoDq>,
+                         (const void*)bwd_main_kernel<D, false, kModeOrderedXcd>,
+                         (const void*)bwd_main_kernel<D, true, kModeAtomic>, (const void*)bwd_main_kernel<D, true, kModeOrdered>,
+                         (const void*)bwd_main_kernel<D, true, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeNoDq>,
+                         (const void*)bwd_main_kernel<D, true, kModeOrderedXcd>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 256, 0) != hipSuccess) return 0;

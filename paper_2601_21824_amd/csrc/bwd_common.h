@@ -78,6 +78,13 @@ __device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint3
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc1 lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r), "s"(soff) : "memory");
 }
+// ... L2-coherent (SC0: the copy skips the CU's L1 and reads the XCD's L2),
+// for data that only workgroups of one XCD write and read
+__device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off, uint32_t soff) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc0 lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r), "s"(soff) : "memory");
+}
 __device__ inline void dma4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
@@ -88,6 +95,13 @@ __device__ inline void dma4_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
 }
+// The XCD (accelerator complex die, with its own L2) this wave runs on.
+__device__ inline int xcc_id() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return (int)(x & 15);
+}
+
 // The lane index, read afresh where it is called.  Per-lane offsets derived
 // from it are rebuilt in a step instead of being hoisted out of the loop and
 // spilled: a spill reload waits for every vector memory operation in flight,

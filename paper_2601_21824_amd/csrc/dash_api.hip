@@ -62,7 +62,7 @@ Layout layout(int B, int H, int N, int d, int sched) {
   L.steps = off;
   off += align256(chains * L.step_cap * sizeof(unsigned));
   L.order = off;
-  off += align256(bh * chains * 2 * sizeof(int));
+  off += align256((bh + dash::kMaxXcd) * chains * 2 * sizeof(int));  // XCD segments round up per XCD
   L.total = off;
   return L;
 }
@@ -71,7 +71,35 @@ struct DeviceInfo {
   int device = -1;
   int cus = 0;
   int occ64 = 0, occ128 = 0, occ256 = 0;
+  int nxcd = 0;  // XCDs, when workgroup i runs on XCD i % nxcd (0: not usable for XCD-local placement)
 };
+
+// Each workgroup records the XCD it runs on.
+__global__ void xcc_probe_kernel(int* out) {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  if (threadIdx.x == 0) out[blockIdx.x] = (int)(x & 15);
+}
+
+// Number of XCDs if the dispatcher deals workgroups out to them round-robin
+// (what the XCD-local placement relies on to give every XCD its share of a
+// persistent grid), else 0.
+int probe_xcds() {
+  constexpr int kWg = 64;
+  int* d = nullptr;
+  if (hipMalloc(&d, kWg * sizeof(int)) != hipSuccess) return 0;
+  int h[kWg];
+  hipLaunchKernelGGL(xcc_probe_kernel, dim3(kWg), dim3(64), 0, nullptr, d);
+  const bool ok = hipGetLastError() == hipSuccess && hipMemcpy(h, d, sizeof(h), hipMemcpyDeviceToHost) == hipSuccess;
+  (void)hipFree(d);
+  if (!ok) return 0;
+  int n = 0;
+  for (int i = 0; i < kWg; ++i) n = h[i] + 1 > n ? h[i] + 1 : n;
+  if (n < 1 || n > dash::kMaxXcd) return 0;
+  for (int i = 0; i < kWg; ++i)
+    if (h[i] != i % n) return 0;
+  return n;
+}
 
 std::mutex g_mu;
 DeviceInfo g_dev[64];
@@ -94,6 +122,7 @@ int device_info(DeviceInfo* out) {
     di.occ128 = dash::bwd_main_occupancy(128);
     di.occ256 = dash::bwd_main_occupancy(256);
     if (di.occ64 <= 0 || di.occ128 <= 0 || di.occ256 <= 0) return fail(DASH_ERR_HIP, "occupancy query failed");
+    di.nxcd = probe_xcds();
     di.device = dev;
   }
   *out = di;
@@ -140,6 +169,37 @@ int check_bwd(const void* q, const void* k, const void* v, const void* o, const 
   if (!q || !k || !v || !o || !dO || !lse || !dq || !dk || !dv)
     return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(DASH_ERR_INVALID_ARG, "scale must be finite and > 0");
+  return DASH_OK;
+}
+
+int occupancy(const DeviceInfo& di, int d) { return d == 64 ? di.occ64 : d == 128 ? di.occ128 : di.occ256; }
+
+// XCD-local placement (every chain of a head on one XCD, see place_on_xcds)
+// serves the ordered schedules when the chains that must run at once fit the
+// workgroups one XCD keeps resident.  AUTO takes it when every XCD gets at
+// least one head (otherwise one queue spreads a few heads over all XCDs) and
+// a caller's workgroup cap leaves every XCD those chains -- except that a cap
+// never changes the summation order: where the placement decides Shift's
+// groups, a cap too small for XCD placement is rejected instead.
+int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, long heads, int want, int max_wg,
+                     bool* xcd) {
+  const bool ordered = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING || sched == DASH_SCHED_SHIFT ||
+                       sched == DASH_SCHED_SYMSHIFT;
+  dash::Geom Gx = dash::make_geom(sched, causal, N, d);
+  dash::place_on_xcds(Gx);
+  const long per_xcd = di.nxcd > 0 ? (long)occupancy(di, d) * di.cus / di.nxcd : 0;
+  const long together = sched == DASH_SCHED_SHIFT ? Gx.grp : sched == DASH_SCHED_SYMSHIFT ? Gx.chains : 1;
+  const bool possible = di.nxcd > 0 && ordered && d <= 128 && together <= per_xcd;
+  const bool order_depends = sched == DASH_SCHED_SHIFT && Gx.chains > dash::kXcdGroup;
+  const bool fits_cap = max_wg <= 0 || max_wg >= together * di.nxcd;
+  if (want == DASH_PLACEMENT_XCD) {
+    if (!possible)
+      return fail(DASH_ERR_UNSUPPORTED, "XCD-local placement needs an ordered schedule, d <= 128 and the co-running "
+                                        "chains within one XCD's resident workgroups");
+    *xcd = true;
+  } else {
+    *xcd = want == DASH_PLACEMENT_AUTO && possible && heads >= di.nxcd && (fits_cap || order_depends);
+  }
   return DASH_OK;
 }
 
@@ -198,15 +258,23 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   const int tickets = opts ? opts->ticket_order : DASH_TICKETS_AUTO;
   if (tickets < DASH_TICKETS_AUTO || tickets > DASH_TICKETS_CHAIN_MAJOR)
     return fail(DASH_ERR_INVALID_ARG, "unknown ticket_order");
+  const int placement = opts ? opts->placement : DASH_PLACEMENT_AUTO;
+  if (placement < DASH_PLACEMENT_AUTO || placement > DASH_PLACEMENT_XCD)
+    return fail(DASH_ERR_INVALID_ARG, "unknown placement");
+  const int sched = resolve(schedule, d, causal);
+  if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
+    return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
   DeviceInfo di;
   if ((rc = device_info(&di))) return rc;
 
-  const int sched = resolve(schedule, d, causal);
   dash::Geom G = dash::make_geom(sched, causal, N, d);
-  if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
-    return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
-  const int occ = d == 64 ? di.occ64 : d == 128 ? di.occ128 : di.occ256;
-  const long resident = (long)occ * di.cus;
+  bool xcd = false;
+  if ((rc = choose_placement(di, sched, causal, N, d, (long)B * H, placement, opts ? opts->max_workgroups : 0, &xcd)))
+    return rc;
+  if (xcd) dash::place_on_xcds(G);
+  const int nq = xcd ? di.nxcd : 1;  // ticket queues; workgroup i serves queue i % nq
+  // workgroups one queue keeps resident
+  const long resident = (long)occupancy(di, d) * di.cus / nq;
   if (tickets != DASH_TICKETS_AUTO) {
     G.chain_major = tickets == DASH_TICKETS_CHAIN_MAJOR;
   } else if (sched != DASH_SCHED_SHIFT && sched != DASH_SCHED_SYMSHIFT) {
@@ -219,8 +287,17 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
     // they go chain-major under a causal mask only.  Once one head's chains
     // fill the GPU, head-major keeps the resident workgroups on one head's
     // Q / dO and wins.  (Measured over d = 64 / 128 / 256 and both masks.)
+    // Under XCD-local placement an XCD's queue holds several heads whose
+    // chains outnumber its resident workgroups: chain-major keeps the naive
+    // pipeline fill short there as well (B=2 N=8192: +7% full, +25% causal),
+    // and for Descending except with a causal mask at d = 128, where its
+    // chains all start at the last Q tile and head-major measured 6% better
+    // (at d = 64 chain-major is 6% better).
     const bool waits = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING;
-    G.chain_major = (long)G.chains < resident && (waits || causal);
+    if (xcd)
+      G.chain_major = sched == DASH_SCHED_NAIVE || (sched == DASH_SCHED_DESCENDING && (!causal || d < 128));
+    else
+      G.chain_major = (long)G.chains < resident && (waits || causal);
   }
   // Shift-type chains wait on each other in a cycle: every chain of a Shift
   // group (Symmetric Shift: of a head) must be able to run at once.  Naive and
@@ -231,14 +308,17 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
     return fail(DASH_ERR_UNSUPPORTED, "too many KV tiles per head for the resident workgroups of this GPU");
   if ((long)(G.t_r + 1) * G.nsub > dash::kMaxChainSteps || N > 32768)
     return fail(DASH_ERR_UNSUPPORTED, "sequence too long for one workgroup chain (N <= 32768)");
-  const long items = (long)B * H * G.chains;
+  // per queue: its work items (XCD queues: the heads bh % nxcd == x, padded
+  // to the largest such set) and at most `resident` workgroups
+  const int xcd_cap = xcd ? ((B * H + nq - 1) / nq) * G.chains : 0;
+  const long items = xcd ? (long)xcd_cap : (long)B * H * G.chains;
   long cap = resident;
   if (opts && opts->max_workgroups > 0) {
-    if (opts->max_workgroups < coresident)
+    if (opts->max_workgroups < coresident * nq)
       return fail(DASH_ERR_INVALID_ARG, "max_workgroups is below the chains that must run at once");
-    if (opts->max_workgroups < cap) cap = opts->max_workgroups;
+    if (opts->max_workgroups / nq < cap) cap = opts->max_workgroups / nq;
   }
-  const int grid = (int)(items < cap ? items : cap);
+  const int grid = (int)(items < cap ? items : cap) * nq;
 
   char* ws = (char*)workspace;
   dash::BwdArgs a;
@@ -259,6 +339,8 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   a.steps = (unsigned*)(ws + L.steps);
   a.step_cap = L.step_cap;
   a.order = (int*)(ws + L.order);
+  a.nxcd = xcd ? di.nxcd : 0;
+  a.xcd_cap = xcd_cap;
   a.witness = opts ? opts->witness : nullptr;
   a.partials = opts ? opts->partials : nullptr;
   a.dq_accum = opts ? opts->dq_accum : nullptr;
@@ -312,6 +394,18 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
   return dash_bwd_check(g_ws, nullptr);
 }
 
+int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if ((rc = check_schedule(schedule, causal))) return rc;
+  DeviceInfo di;
+  if ((rc = device_info(&di))) return rc;
+  bool xcd = false;
+  if ((rc = choose_placement(di, resolve(schedule, d, causal), causal, N, d, (long)B * H, DASH_PLACEMENT_AUTO, 0, &xcd)))
+    return rc;
+  return xcd ? DASH_PLACEMENT_XCD : DASH_PLACEMENT_GLOBAL;
+}
+
 void dash_release_workspace(void) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   if (g_ws) (void)hipFree(g_ws);
@@ -319,13 +413,16 @@ void dash_release_workspace(void) {
   g_ws_bytes = 0;
 }
 
-int dash_schedule_table(int schedule, int N, int d, int causal, int* geometry, int* chain_len, int* task_kv,
-                        int* task_q, int* rank) {
+int dash_schedule_table(int schedule, int N, int d, int causal, int placement, int* geometry, int* chain_len,
+                        int* task_kv, int* task_q, int* rank) {
   int rc = check_shape(1, 1, N, d);
   if (rc) return rc;
   if ((rc = check_schedule(schedule, causal))) return rc;
+  if (placement != DASH_PLACEMENT_GLOBAL && placement != DASH_PLACEMENT_XCD)
+    return fail(DASH_ERR_INVALID_ARG, "placement must be DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD");
   const int sched = resolve(schedule, d, causal);
-  const dash::Geom G = dash::make_geom(sched, causal, N, d);
+  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  if (placement == DASH_PLACEMENT_XCD) dash::place_on_xcds(G);
   if (geometry) {
     geometry[0] = G.t_r;
     geometry[1] = G.t_c;

@@ -11,6 +11,8 @@ constexpr int kCtrStride = 32;        // ints per ordering counter (one 128-byte
 constexpr int kPoison = -0x40000000;  // counter start value below every rank's turn
 constexpr int kCtrlTicket = 0;        // ctrl[] slot: next work item
 constexpr int kCtrlError = 16;        // ctrl[] slot: set to 1 when a wait timed out
+constexpr int kCtrlXcdTicket = 32;    // ctrl[] slots 32 + x: next work item of XCD x (XCD-local placement)
+constexpr int kMaxXcd = 16;           // XCD queues the ctrl block holds
 constexpr size_t kCtrlBytes = 256;    // ctrl block at the start of the workspace
 constexpr int kMaxChainSteps = 1040;  // 64-row blocks one workgroup chain may visit
 
@@ -29,6 +31,7 @@ constexpr int kModeAtomic = 0;    // fp32 atomic adds into dQacc (non-determinis
 constexpr int kModeOrdered = 1;   // the ordered reduction (every DASH schedule)
 constexpr int kModePartials = 2;  // store it in its own buffer; bwd_sum_partials adds them in KV order
 constexpr int kModeNoDq = 3;      // no dQ at all: dK, dV only (SPLIT's first pass)
+constexpr int kModeOrderedXcd = 4;  // the ordered reduction with every head on one XCD (L2-local accumulator)
 
 struct BwdArgs {
   const void* q;
@@ -47,7 +50,10 @@ struct BwdArgs {
   int* ctrl;      // ticket / error flag
   unsigned* steps;  // [chains][step_cap]: per chain its length, then its packed steps (bwd_pre writes them)
   int step_cap;
-  int* order;       // [bh * chains][2]: work ticket -> (head, chain) (bwd_pre writes it)
+  int* order;       // [items][2]: work ticket -> (head, chain) (bwd_pre writes it); XCD-local
+                   // placement: XCD x's tickets at [x * xcd_cap, x * xcd_cap + its items)
+  int nxcd;         // XCD-local placement: number of XCDs (head bh runs on XCD bh % nxcd); 0: one queue
+  int xcd_cap;      // work items per XCD segment of `order`
   int32_t* witness;
   float* partials;
   float* dq_accum;

@@ -48,6 +48,7 @@ enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIF
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
 constexpr int kTileKV = 128;    // KV rows per tile of the d = 64 / 128 kernel
 constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident
+constexpr int kXcdGroup = 32;   // ... under XCD-local placement (one XCD's resident workgroups)
 
 struct Geom {
   int sched;   // Sched
@@ -138,6 +139,33 @@ DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
       *i = first_q(G, w) + t;
       return;
   }
+}
+
+// XCD-local placement: every chain of head bh runs on XCD bh % nxcd, so the
+// head's dQ accumulator and counters stay in that XCD's L2.  A Shift group
+// must then fit one XCD's resident workgroups: groups of at most kXcdGroup
+// chains, which the XCD runs one after another (the group-major order of
+// rank_of).  The other schedules' orders do not depend on the placement.
+DASH_HD void place_on_xcds(Geom& G) {
+  if (G.sched == S_SHIFT && G.grp > kXcdGroup) G.grp = kXcdGroup;
+}
+
+// heads of XCD x (of nxcd) under XCD-local placement: x, x + nxcd, ...
+DASH_HD int xcd_heads(int heads, int nxcd, int x) { return x < heads ? (heads - x + nxcd - 1) / nxcd : 0; }
+
+// XCD x's work ticket t -> (head, chain), head-major or chain-major over the
+// XCD's own heads as ticket_chain
+DASH_HD void ticket_chain_xcd(const Geom& G, int heads, int nxcd, int x, int t, int* bh, int* w) {
+  const int hx = xcd_heads(heads, nxcd, x);
+  int k;
+  if (G.chain_major) {
+    *w = t / hx;
+    k = t % hx;
+  } else {
+    k = t / G.chains;
+    *w = t % G.chains;
+  }
+  *bh = x + nxcd * k;
 }
 
 // Work ticket -> (head, chain).  Head-major (all chains of a head in a row,

@@ -68,6 +68,12 @@ def test_argument_errors_without_device():
     rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
                               1 << 40, ctypes.byref(opts), None)
     assert rc == b.DASH_ERR_INVALID_ARG and "ticket_order" in b.dash_last_error()
+    # ... and so is an unknown placement
+    opts = b.dash_bwd_options_t(0, 0, None, None, None, None, None, 0, 0, 3)
+    rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
+                              1 << 40, ctypes.byref(opts), None)
+    assert rc == b.DASH_ERR_INVALID_ARG and "placement" in b.dash_last_error()
+    assert lib.dash_schedule_table(1, 128, 64, 0, 0, None, None, None, None, None) == b.DASH_ERR_INVALID_ARG
 
 
 def test_schedule_resolution():
@@ -86,22 +92,25 @@ KINDS = {b.DASH_SCHED_NAIVE: osched.NAIVE, b.DASH_SCHED_DESCENDING: osched.DESCE
          b.DASH_SCHED_SPLIT: osched.NAIVE}
 
 
+@pytest.mark.parametrize("placement", [b.DASH_PLACEMENT_GLOBAL, b.DASH_PLACEMENT_XCD])
 @pytest.mark.parametrize("d", [64, 128, 256])
-@pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 8192, 16384, 32768])
+@pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 4224, 8192, 16384, 32768])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("sched", [0, 1, 2, 3, 4, 6, 7])
-def test_schedule_table_matches_oracle(sched, causal, N, d):
+def test_schedule_table_matches_oracle(sched, causal, N, d, placement):
     if sched == b.DASH_SCHED_SYMSHIFT and not causal:
         pytest.skip("symshift is causal-only")
-    tab = b.dash_schedule_table(sched, N, d, causal)
+    tab = b.dash_schedule_table(sched, N, d, causal, placement)
     concrete = b.dash_resolve_schedule(sched, d, causal)
     kind = KINDS[concrete]
     t_r, t_c, br, bc, grp = tab["t_r"], tab["t_c"], tab["br"], tab["bc"], tab["group"]
     # tile sizes: KV tiles of 128 rows (64 at d = 256); Q tiles of 64 rows (full)
-    # or KV-tile rows (causal); Shift groups of at most 256 chains
+    # or KV-tile rows (causal); Shift groups of at most 256 chains, 32 when every
+    # chain of a head runs on one XCD
     assert bc == (128 if d <= 128 else 64)
     assert br == (bc if causal else 64) and t_r * br == t_c * bc
-    assert grp == (min(t_c, 256) if kind == osched.SHIFT else tab["chains"])
+    most = 32 if placement == b.DASH_PLACEMENT_XCD else 256
+    assert grp == (min(t_c, most) if kind == osched.SHIFT else tab["chains"])
     ref = osched.build(kind, t_r, t_c, causal, br, bc, group=grp if kind == osched.SHIFT else None)
     assert tab["chains"] == len(ref.chains)
     for w, ch in enumerate(ref.chains):

@@ -103,38 +103,48 @@ def test_partials_variant_equals_naive_bitwise(N, d, causal):
         assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
 
 
+GL, XL = 1, 2  # DASH_PLACEMENT_GLOBAL, DASH_PLACEMENT_XCD
 PROTO_CASES = [
-    (1, 2, 512, 128, False, "shift"),
-    (1, 2, 512, 128, False, "naive"),
-    (1, 2, 576, 64, True, "symshift"),
-    (1, 2, 512, 128, True, "symshift"),
-    (1, 2, 512, 128, True, "descending"),
-    (2, 1, 300, 64, True, "symshift"),
-    (2, 1, 300, 128, False, "shift"),
-    (1, 2, 512, 256, False, "shift"),
-    (1, 2, 512, 256, True, "symshift"),
-    (1, 1, 333, 256, True, "descending"),
+    (1, 2, 512, 128, False, "shift", GL),
+    (1, 2, 512, 128, False, "naive", GL),
+    (1, 2, 576, 64, True, "symshift", GL),
+    (1, 2, 512, 128, True, "symshift", GL),
+    (1, 2, 512, 128, True, "descending", GL),
+    (2, 1, 300, 64, True, "symshift", GL),
+    (2, 1, 300, 128, False, "shift", GL),
+    (1, 2, 512, 256, False, "shift", GL),
+    (1, 2, 512, 256, True, "symshift", GL),
+    (1, 1, 333, 256, True, "descending", GL),
+    # every chain of a head on one XCD (L2-local accumulator); at 33 KV tiles
+    # Shift runs as two groups, 32 chains then 1
+    (1, 2, 4224, 128, False, "shift", XL),
+    (3, 3, 700, 64, False, "shift", XL),
+    (1, 2, 576, 64, True, "symshift", XL),
+    (2, 5, 512, 128, True, "descending", XL),
+    (2, 1, 300, 128, False, "naive", XL),
 ]
 
 
-@pytest.mark.parametrize("case", PROTO_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in PROTO_CASES])
+@pytest.mark.parametrize("case", PROTO_CASES,
+                         ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}-{'xcd' if c[6] == XL else 'global'}"
+                              for c in PROTO_CASES])
 def test_witness_and_partial_sum_replay(case):
     """The order the workgroups actually added their partials in equals the
     oracle's order, and summing the exported partials in that order in fp32
     reproduces the accumulator bit for bit (and dQ = bf16(scale * acc))."""
-    B, H, N, d, causal, sched = case
+    B, H, N, d, causal, sched, placement = case
     print(f"\n[protocol] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=21)
     og, lseg = run_fwd(qg, kg, vg, causal)
     nblk = (N + 63) // 64
-    tab = dash.dash_schedule_table(sched, N, d, causal)
+    tab = dash.dash_schedule_table(sched, N, d, causal, placement)
     tc = (N + tab["bc"] - 1) // tab["bc"]  # KV tiles (before Symmetric Shift's padding)
     witness = torch.full((B * H, nblk, tc), -1, dtype=torch.int32, device="cuda")
     partials = torch.full((B * H, tc, N, d), float("nan"), dtype=torch.float32, device="cuda")
     acc = torch.full((B * H, N, d), float("nan"), dtype=torch.float32, device="cuda")
-    opts = dash.dash_bwd_options_t(0, 0, witness.data_ptr(), partials.data_ptr(), acc.data_ptr(), None, None)
+    opts = dash.dash_bwd_options_t(0, 0, witness.data_ptr(), partials.data_ptr(), acc.data_ptr(), None, None,
+                                   0, 0, placement)
     dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts)
-    tab = dash.dash_schedule_table(sched, N, d, causal)
     kind = {"shift": osched.SHIFT, "naive": osched.NAIVE, "descending": osched.DESCENDING,
             "symshift": osched.SYMSHIFT}[sched]
     ref = osched.build(kind, tab["t_r"], tab["t_c"], causal, tab["br"], tab["bc"],
@@ -227,6 +237,72 @@ def test_ticket_order_does_not_change_bits(case):
             run_bwd(qg, kg, vg, og, dog, lseg, causal, s, workspace=dash.new_workspace(B, H, N, d, s),
                     options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 0,
                                                     dash.DASH_TICKETS_CHAIN_MAJOR))
+        assert e.value.code == dash.DASH_ERR_INVALID_ARG
+
+
+PLACE_CASES = [
+    (2, 8, 2048, 128, False, "naive"),
+    (2, 8, 2048, 128, True, "descending"),
+    (2, 8, 4096, 128, False, "shift"),
+    (2, 8, 2048, 128, True, "symshift"),
+    (4, 4, 1024, 64, True, "symshift"),
+    (1, 8, 8192, 64, True, "descending"),
+    (2, 4, 6144, 128, False, "shift"),
+]
+
+
+@pytest.mark.parametrize("case", PLACE_CASES, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}"
+                                                    for c in PLACE_CASES])
+def test_placement(case):
+    """XCD-local placement (each head's chains, accumulator and counters on one
+    XCD) against one global queue: bitwise the same result wherever the
+    schedule's order does not depend on the placement (all but Shift with more
+    than 32 KV tiles, whose groups shrink to 32 chains); there the witnessed
+    order is the oracle's with groups of 32, and the result is deterministic.
+    AUTO takes XCD placement for B*H >= the XCD count, and a workgroup cap
+    below one XCD's co-running chains per XCD falls back to the global queue
+    where that leaves the bits unchanged."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[placement] {case}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=23)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d, sched)
+    assert dash.dash_bwd_placement(B, H, N, d, causal, sched) == XL
+    place = lambda p, cap=0: dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap, 0, p)
+    auto = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    xcd = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(XL))
+    glob = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(GL))
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    for a_, b_ in zip(auto, xcd):
+        assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+    tab_x = dash.dash_schedule_table(sched, N, d, causal, XL)
+    tab_g = dash.dash_schedule_table(sched, N, d, causal, GL)
+    if tab_x["group"] == tab_g["group"]:
+        for a_, b_ in zip(xcd, glob):
+            assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+        # a cap of 3 workgroups: the global queue, same bits
+        small = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(0, 3)) \
+            if sched in ("naive", "descending") else None
+        if small is not None:
+            for a_, b_ in zip(xcd, small):
+                assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+    else:
+        nblk = (N + 63) // 64
+        witness = torch.full((B * H, nblk, tab_x["t_c"]), -1, dtype=torch.int32, device="cuda")
+        opts = dash.dash_bwd_options_t(0, 0, witness.data_ptr(), None, None, None, None, 0, 0, XL)
+        again = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts)
+        for a_, b_ in zip(xcd, again):
+            assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+        order = osched.build(osched.SHIFT, tab_x["t_r"], tab_x["t_c"], causal, tab_x["br"], tab_x["bc"],
+                             group=tab_x["group"]).order
+        W = witness.cpu().numpy()
+        for bh in range(B * H):
+            for pb in range(nblk):
+                assert W[bh, pb].tolist() == order[pb], (bh, pb)
+        # the groups are part of the order: a cap too small for them is rejected
+        with pytest.raises(dash.DashError) as e:
+            run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(0, 3))
         assert e.value.code == dash.DASH_ERR_INVALID_ARG
 
 
