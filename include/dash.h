@@ -144,11 +144,11 @@ typedef struct {
    device-coherent path.  Each XCD takes work from its own ticket queue; a
    Shift group is then at most 32 chains (what one XCD keeps resident), and a
    head's groups run one after another.  Ordered schedules (naive, Descending,
-   Shift, Symmetric Shift) at d = 64 and 128, when the chains that must run at
-   once fit one XCD (Symmetric Shift: T_c <= 64).
+   Shift, Symmetric Shift), when the chains that must run at once fit one XCD
+   (Symmetric Shift: T_c <= 64).
    GLOBAL: one ticket queue for the whole GPU (any schedule, any d).
-   AUTO: XCD when it is possible and B*H is at least the number of XCDs, else
-   GLOBAL (dash_bwd_placement tells which). */
+   AUTO: XCD when it is possible, B*H is at least the number of XCDs and (for
+   Shift) T_c <= 256, else GLOBAL (dash_bwd_placement tells which). */
 #define DASH_PLACEMENT_AUTO 0
 #define DASH_PLACEMENT_GLOBAL 1
 #define DASH_PLACEMENT_XCD 2

@@ -57,7 +57,7 @@ struct Smem256 {
   int item;
 };
 
-template <bool CAUSAL, bool ORDERED>
+template <bool CAUSAL, bool ORDERED, bool XCD>
 __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) Smem256 sm;
 
@@ -67,8 +67,14 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const float c2 = a.scale * kLog2e;
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
-  const int total = a.bh * G.chains;
   constexpr bool ordered = ORDERED;  // false: the atomic variant
+  // XCD-local placement (ordered only): the heads of this XCD from its own
+  // ticket queue, the accumulator through the XCD's L2
+  constexpr bool xcd = XCD;
+  const int xq = xcd ? xcc_id() : 0;
+  const int total = xcd ? (xq < a.nxcd ? xcd_heads(a.bh, a.nxcd, xq) * G.chains : 0) : a.bh * G.chains;
+  int* const ticket = &a.ctrl[xcd ? kCtrlXcdTicket + xq : kCtrlTicket];
+  const int* const order = a.order + (xcd ? 2 * xq * a.xcd_cap : 0);
   // Shift-type orders are conflict-free: the next contributor to a block comes
   // at least one step later, so the counter release can wait until the next
   // step's dV/dK work has covered the store latency.
@@ -76,14 +82,14 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   bool failed = false;
 
   for (;;) {
-    if (tid == 0) sm.item = atomicAdd(&a.ctrl[kCtrlTicket], 1);
+    if (tid == 0) sm.item = atomicAdd(ticket, 1);
     __syncthreads();
     const int item = __builtin_amdgcn_readfirstlane(sm.item);  // wave-uniform (SGPR)
     if (item >= total) break;
     // (head, chain) of the ticket from bwd_pre's table; wave-uniform, so the
     // head's buffer descriptors stay in SGPRs
-    const int bh = __builtin_amdgcn_readfirstlane(a.order[2 * item]);
-    const int wch = __builtin_amdgcn_readfirstlane(a.order[2 * item + 1]);
+    const int bh = __builtin_amdgcn_readfirstlane(order[2 * item]);
+    const int wch = __builtin_amdgcn_readfirstlane(order[2 * item + 1]);
     const size_t head = (size_t)bh * N * D;
     const auto rq = make_rsrc((const __bf16*)a.q + head, hbytes);
     const auto rk = make_rsrc((const __bf16*)a.k + head, hbytes);
@@ -134,7 +140,10 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
     auto acc_off = [&](int pb, int t) { return (uint32_t)(pb * BM * D + w * 4096 + t * 256 + 4 * l) * 4; };
     auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int t = 0; t < 16; ++t) lds_load16_coherent(racc, &acc_w[t * 256], acc_off(pb, t));
+      for (int t = 0; t < 16; ++t) {
+        if constexpr (xcd) lds_load16_l2(racc, &acc_w[t * 256], acc_off(pb, t));
+        else lds_load16_coherent(racc, &acc_w[t * 256], acc_off(pb, t));
+      }
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -382,7 +391,8 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
               st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
               if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
             } else {
-              st16_coherent(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
+              if constexpr (xcd) st16(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
+              else st16_coherent(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
             }
           }
         }
@@ -421,18 +431,21 @@ void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream) {
   const bool atomic = a.G.sched == S_ATOMIC;
   const dim3 grid(grid_main), block(NT);
   if (a.G.causal) {
-    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<true, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main256_kernel<true, true>), grid, block, 0, stream, a);
+    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<true, false, false>), grid, block, 0, stream, a);
+    else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<true, true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((bwd_main256_kernel<true, true, false>), grid, block, 0, stream, a);
   } else {
-    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<false, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main256_kernel<false, true>), grid, block, 0, stream, a);
+    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<false, false, false>), grid, block, 0, stream, a);
+    else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<false, true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((bwd_main256_kernel<false, true, false>), grid, block, 0, stream, a);
   }
 }
 
 int bwd_main256_occupancy() {
   int lo = 1 << 30;
-  const void* fns[4] = {(const void*)bwd_main256_kernel<false, false>, (const void*)bwd_main256_kernel<false, true>,
-                        (const void*)bwd_main256_kernel<true, false>, (const void*)bwd_main256_kernel<true, true>};
+  const void* fns[6] = {(const void*)bwd_main256_kernel<false, false, false>, (const void*)bwd_main256_kernel<false, true, false>,
+                        (const void*)bwd_main256_kernel<false, true, true>, (const void*)bwd_main256_kernel<true, false, false>,
+                        (const void*)bwd_main256_kernel<true, true, false>, (const void*)bwd_main256_kernel<true, true, true>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, NT, 0) != hipSuccess) return 0;

@@ -45,6 +45,9 @@ __device__ inline void lds_load16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t 
 __device__ inline void lds_load16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, kCoherent);
 }
+__device__ inline void lds_load16_l2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC0: the XCD's L2
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, 1);
+}
 __device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
 }

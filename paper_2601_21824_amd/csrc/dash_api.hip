@@ -177,7 +177,8 @@ int occupancy(const DeviceInfo& di, int d) { return d == 64 ? di.occ64 : d == 12
 // XCD-local placement (every chain of a head on one XCD, see place_on_xcds)
 // serves the ordered schedules when the chains that must run at once fit the
 // workgroups one XCD keeps resident.  AUTO takes it when every XCD gets at
-// least one head (otherwise one queue spreads a few heads over all XCDs) and
+// least one head (otherwise one queue spreads a few heads over all XCDs), a
+// Shift head has at most 8 groups, and
 // a caller's workgroup cap leaves every XCD those chains -- except that a cap
 // never changes the summation order: where the placement decides Shift's
 // groups, a cap too small for XCD placement is rejected instead.
@@ -189,16 +190,19 @@ int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, 
   dash::place_on_xcds(Gx);
   const long per_xcd = di.nxcd > 0 ? (long)occupancy(di, d) * di.cus / di.nxcd : 0;
   const long together = sched == DASH_SCHED_SHIFT ? Gx.grp : sched == DASH_SCHED_SYMSHIFT ? Gx.chains : 1;
-  const bool possible = di.nxcd > 0 && ordered && d <= 128 && together <= per_xcd;
+  const bool possible = di.nxcd > 0 && ordered && together <= per_xcd;
   const bool order_depends = sched == DASH_SCHED_SHIFT && Gx.chains > dash::kXcdGroup;
   const bool fits_cap = max_wg <= 0 || max_wg >= together * di.nxcd;
   if (want == DASH_PLACEMENT_XCD) {
     if (!possible)
-      return fail(DASH_ERR_UNSUPPORTED, "XCD-local placement needs an ordered schedule, d <= 128 and the co-running "
-                                        "chains within one XCD's resident workgroups");
+      return fail(DASH_ERR_UNSUPPORTED, "XCD-local placement needs an ordered schedule and the co-running chains "
+                                        "within one XCD's resident workgroups");
     *xcd = true;
   } else {
-    *xcd = want == DASH_PLACEMENT_AUTO && possible && heads >= di.nxcd && (fits_cap || order_depends);
+    // measured: XCD placement is as fast or faster everywhere except Shift
+    // heads of more than 8 groups (d = 256, N = 32768: 7% slower)
+    const bool worth = !(sched == DASH_SCHED_SHIFT && Gx.t_c > 8 * dash::kXcdGroup);
+    *xcd = want == DASH_PLACEMENT_AUTO && possible && worth && heads >= di.nxcd && (fits_cap || order_depends);
   }
   return DASH_OK;
 }

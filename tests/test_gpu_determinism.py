@@ -248,6 +248,9 @@ PLACE_CASES = [
     (4, 4, 1024, 64, True, "symshift"),
     (1, 8, 8192, 64, True, "descending"),
     (2, 4, 6144, 128, False, "shift"),
+    (1, 8, 4096, 256, False, "shift"),
+    (1, 8, 2048, 256, True, "descending"),
+    (2, 4, 2048, 256, True, "symshift"),
 ]
 
 
