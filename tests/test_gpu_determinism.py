@@ -177,29 +177,29 @@ GRID_CASES = [
 
 @pytest.mark.parametrize("case", GRID_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in GRID_CASES])
 def test_grid_size_does_not_change_bits(case):
-    """The summation order is a function of the schedule and shape only: the
-    persistent grid's size (from one head's chains up to the GPU's resident
-    count) leaves every output bit unchanged; below one head's chains the call
-    is rejected."""
+    """The summation order is a function of the schedule, shape and placement
+    only: the persistent grid's size (from the chains that must run at once --
+    per XCD under XCD-local placement -- up to the GPU's resident count)
+    leaves every output bit unchanged; below that the call is rejected."""
     B, H, N, d, causal, sched = case
     print(f"\n[grid] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=31)
     og, lseg = run_fwd(qg, kg, vg, causal)
-    tab = dash.dash_schedule_table(sched, N, d, causal)
-    chains = tab["group"] if sched in ("shift", "symshift") else 1
     ws = dash.new_workspace(B, H, N, d)
-    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
-    for cap in (max(chains, 2), chains + 3, 2 * tab["chains"] + 1):
-        opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap)
-        got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts, workspace=ws)
-        assert dash.dash_bwd_check(ws) == dash.DASH_OK
-        for a, b in zip(ref, got):
-            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"grid {cap} differs"
-    if chains > 1:
-        with pytest.raises(dash.DashError) as e:
-            run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws,
-                    options=dash.dash_bwd_options_t(0, 0, None, None, None, None, None, chains - 1))
-        assert e.value.code == dash.DASH_ERR_INVALID_ARG
+    for place, queues in ((GL, 1), (XL, 8)):  # MI355X: 8 XCDs, one queue each
+        tab = dash.dash_schedule_table(sched, N, d, causal, place)
+        together = (tab["group"] if sched in ("shift", "symshift") else 1) * queues
+        opts = lambda cap: dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap, 0, place)
+        ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts(0))
+        for cap in (max(together, 2), together + 3, 2 * together + 1):
+            got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, options=opts(cap), workspace=ws)
+            assert dash.dash_bwd_check(ws) == dash.DASH_OK
+            for a, b in zip(ref, got):
+                assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"placement {place} grid {cap} differs"
+        if together > 1:
+            with pytest.raises(dash.DashError) as e:
+                run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts(together - 1))
+            assert e.value.code == dash.DASH_ERR_INVALID_ARG
 
 
 TICKET_CASES = [
@@ -257,11 +257,11 @@ PLACE_CASES = [
 @pytest.mark.parametrize("case", PLACE_CASES, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}"
                                                     for c in PLACE_CASES])
 def test_placement(case):
-    """XCD-local placement (each head's chains, accumulator and counters on one
-    XCD) against one global queue: bitwise the same result wherever the
-    schedule's order does not depend on the placement (all but Shift with more
-    than 32 KV tiles, whose groups shrink to 32 chains); there the witnessed
-    order is the oracle's with groups of 32, and the result is deterministic.
+    """XCD-local placement (each head's chains and accumulator on one XCD)
+    against one global queue: bitwise the same result wherever the schedule's
+    order does not depend on the placement (all but Shift with more than 32
+    KV tiles, whose groups shrink to 32 chains); there the witnessed order is
+    the oracle's with groups of 32, and the result is deterministic.
     AUTO takes XCD placement for B*H >= the XCD count, and a workgroup cap
     below one XCD's co-running chains per XCD falls back to the global queue
     where that leaves the bits unchanged."""
@@ -281,7 +281,7 @@ def test_placement(case):
         assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
     tab_x = dash.dash_schedule_table(sched, N, d, causal, XL)
     tab_g = dash.dash_schedule_table(sched, N, d, causal, GL)
-    if tab_x["group"] == tab_g["group"]:
+    if np.array_equal(tab_x["rank"], tab_g["rank"]):
         for a_, b_ in zip(xcd, glob):
             assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
         # a cap of 3 workgroups: the global queue, same bits
