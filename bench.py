@@ -213,6 +213,8 @@ def main():
         return
     ms, main_ms, tflops = results[det]
     main_tflops = flops / (main_ms * 1e-3) / 1e12
+    placement = "global" if det == "atomic" else \
+        ("XCD-local" if dash.dash_bwd_placement(B, H, N, d, causal, det) == dash.DASH_PLACEMENT_XCD else "global")
     out = {
         "metric": "deterministic attn-bwd TFLOPS (bf16, d=128, N=8192) + % of atomic variant",
         "value": round(tflops, 2),
@@ -234,7 +236,8 @@ def main():
         "atomic_tflops": round(results["atomic"][2], 2),
         "naive_tflops": round(results["naive"][2], 2) if "naive" in results else None,
         "roofline": {"bound": "mfma", "kernel": f"bwd_main{'256' if d == 256 else ''}_kernel<{d}, "
-                               f"{'causal' if causal else 'full'} mask, {'atomic' if det == 'atomic' else 'ordered'}>",
+                               f"{'causal' if causal else 'full'} mask, {'atomic' if det == 'atomic' else 'ordered'}>"
+                               f", placement {placement}",
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic() if (N, d, causal, det) == (8192, 128, False, "shift") else None,
