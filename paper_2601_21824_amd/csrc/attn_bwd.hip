@@ -21,6 +21,8 @@
 //            The grid is persistent: workgroups take work items from a ticket
 //            counter in order, so every item a wait depends on has been started.
 // bwd_post : atomic variant only: dQ = bf16(s * dQacc).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 #include "bwd_common.h"
@@ -219,6 +221,13 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const int total = xcd ? (xq < a.nxcd ? xcd_heads(a.bh, a.nxcd, xq) * G.chains : 0) : a.bh * G.chains;
   int* const ticket = &a.ctrl[xcd ? kCtrlXcdTicket + xq : kCtrlTicket];
   const int* const order = a.order + (xcd ? 2 * xq * a.xcd_cap : 0);
+  // LDS byte addresses for the direct copies: the base once, offsets as
+  // integers (no generic-to-LDS pointer conversion per copy)
+  const uint32_t sm_lds = lds_base(&sm);
+  auto lds_of = [&](const void* p) { return sm_lds + (uint32_t)((const char*)p - (const char*)&sm); };
+  // L * log2(e) and D of every row of every head (row bh * N + r)
+  const auto rls = make_rsrc(a.lse2, (uint32_t)((size_t)a.bh * N * 4));
+  const auto rds = make_rsrc(a.dvec, (uint32_t)((size_t)a.bh * N * 4));
   // Shift-type orders are conflict-free: the next contributor to a block reaches
   // it at least one step later, so the counter release can wait until the next
   // step's barrier, by which time the accumulator stores have drained.
@@ -270,12 +279,13 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     auto load_part = [&](int pb, int b, int k) {  // part k < QLD of the Q and dO rows
       const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ tile_swz<D>(r);
       const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
-      dma16(rq, &sm.qs[b][(k * NT + 64 * w) * 8], off);
-      dma16(rdo, &sm.dos[b][(k * NT + 64 * w) * 8], off);
+      dma16(rq, lds_of(&sm.qs[b][(k * NT + 64 * w) * 8]), off);
+      dma16(rdo, lds_of(&sm.dos[b][(k * NT + 64 * w) * 8]), off);
     };
     auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
-      if (w == 0) dma4(make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4), &sm.ls[b][0], (uint32_t)(pb * BM + fresh_lane()) * 4);
-      if (w == 1) dma4(make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4), &sm.ds[b][0], (uint32_t)(pb * BM + fresh_lane()) * 4);
+      const uint32_t row = (uint32_t)(bh * N + pb * BM + fresh_lane());  // < 2^30 (checked by the library)
+      if (w == 0) dma4(rls, lds_of(&sm.ls[b][0]), row * 4);
+      if (w == 1) dma4(rds, lds_of(&sm.ds[b][0]), row * 4);
     };
     auto load_block = [&](int pb, int b) {
 #pragma unroll
@@ -293,10 +303,10 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     // block pb's counter into this wave's poll slot.  The counters stay
     // device-coherent under XCD-local placement too: the atomic adds are
     // performed past the L2, so an L2 read of a counter can stay stale.
-    auto poll_copy = [&](int pb) { dma4_coherent(rctr, &sm.poll[w][0], (uint32_t)pb * kCtrStride * 4); };
+    auto poll_copy = [&](int pb) { dma4_coherent(rctr, lds_of(&sm.poll[w][0]), (uint32_t)pb * kCtrStride * 4); };
     auto acc_copy = [&](int pb, int k) {  // chunk k of the slice into its landing pad
-      if constexpr (xcd) dma16_l2(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
-      else dma16_coherent(racc, &acc_w[k * 256], acc_off(pb, 0), (uint32_t)k * 1024);
+      if constexpr (xcd) dma16_l2(racc, lds_of(&acc_w[k * 256]), acc_off(pb, 0), (uint32_t)k * 1024);
+      else dma16_coherent(racc, lds_of(&acc_w[k * 256]), acc_off(pb, 0), (uint32_t)k * 1024);
     };
     auto load_acc = [&](int pb) {
 #pragma unroll
@@ -629,19 +639,21 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           //      slice arrives (LDS landing pad) and leaves in 1 KB coalesced rows.
           //      Each element is touched by exactly one lane: the sum order is the
           //      schedule's.
-          if (have_turn) {
-            const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
+          // (`add` and `last` are wave-uniform: one straight path each)
+          auto finish = [&](auto add_c, auto last_c) {
+            constexpr bool kAdd = decltype(add_c)::value, kLast = decltype(last_c)::value;
             f32x4 old[NACC];
+            if constexpr (kAdd) {
   #pragma unroll
-            for (int k = 0; k < NACC; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+              for (int k = 0; k < NACC; ++k) old[k] = *(const f32x4*)&acc_w[k * 256 + 4 * l];
+            }
   #pragma unroll
             for (int k = 0; k < NACC; ++k) {
               const int t = k >> 2, rb = k & 3;
               f32x4 v = {dq[t][4 * rb], dq[t][4 * rb + 1], dq[t][4 * rb + 2], dq[t][4 * rb + 3]};
-              const f32x4 sum = old[k] + v;
-  #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = add ? sum[e] : v[e];
-              if (last) {
+              if constexpr (kAdd) v = old[k] + v;
+              if constexpr (kLast) {
+                const auto rdq = make_rsrc((__bf16*)a.dq + head, hbytes);
                 const uint32_t off = (uint32_t)((q0 + 32 * (qh0 + t) + lc) * D + 32 * dblk + 8 * rb + 4 * g);
                 st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
                 if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
@@ -649,6 +661,17 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
                 if constexpr (xcd) st16(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
                 else st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
               }
+            }
+          };
+          using T_ = std::true_type;
+          using F_ = std::false_type;
+          if (have_turn) {
+            if (!last) {
+              if (add) finish(T_{}, F_{});
+              else finish(F_{}, F_{});
+            } else {
+              if (add) finish(T_{}, T_{});
+              else finish(F_{}, T_{});
             }
             vm_poll += last ? (a.dq_accum ? 2 * NACC : NACC) : NACC;
           }

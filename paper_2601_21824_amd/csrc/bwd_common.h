@@ -60,43 +60,41 @@ __device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t o
 // and the accumulator fetch in the middle of a step.  With these, the caller
 // owns the ordering: before reading the landed bytes it waits with
 // s_waitcnt vmcnt (vm_wait, vm_wait_le), and a workgroup barrier follows when
-// other waves read them.  m0 (the LDS base of the copy) is saved and restored.
+// other waves read them.  `lds` is the wave-uniform LDS byte address of the
+// copy (lane i writes bytes [lds + 16i, lds + 16i + 16)); m0 is saved and
+// restored around it.
 __device__ inline uint32_t lds_base(const void* p) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p);
 }
-__device__ inline void dma16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+__device__ inline void dma16(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+               : "=&s"(save) : "s"(lds), "v"(off), "s"(r) : "memory");
 }
-__device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC1: device-coherent
-  uint32_t save;
-  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
-}
-// ... with a wave-uniform byte offset added in the scalar offset field, so a
-// run of copies at fixed strides shares one per-lane offset register
-__device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off, uint32_t soff) {
+// ... device-coherent (SC1), with a wave-uniform byte offset added in the
+// scalar offset field, so a run of copies at fixed strides shares one
+// per-lane offset register
+__device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off, uint32_t soff) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc1 lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r), "s"(soff) : "memory");
+               : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");
 }
 // ... L2-coherent (SC0: the copy skips the CU's L1 and reads the XCD's L2),
 // for data that only workgroups of one XCD write and read
-__device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off, uint32_t soff) {
+__device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off, uint32_t soff) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc0 lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r), "s"(soff) : "memory");
+               : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");
 }
-__device__ inline void dma4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+__device__ inline void dma4(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+               : "=&s"(save) : "s"(lds), "v"(off), "s"(r) : "memory");
 }
-__device__ inline void dma4_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC1: device-coherent
+__device__ inline void dma4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off) {  // SC1: device-coherent
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen sc1 lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds_base(dst)), "v"(off), "s"(r) : "memory");
+               : "=&s"(save) : "s"(lds), "v"(off), "s"(r) : "memory");
 }
 // The XCD (accelerator complex die, with its own L2) this wave runs on.
 __device__ inline int xcc_id() {
