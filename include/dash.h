@@ -15,7 +15,7 @@
  *  - Self-attention only: N queries attend to N keys.  With causal != 0,
  *    query i sees key j iff j <= i.
  *  - d must be 64, 128 or 256.  N >= 0 is arbitrary (ragged last tiles are masked);
- *    B, H >= 0.  A problem with B*H*N == 0 is a successful no-op.
+ *    B, H >= 0, B*H*N < 2^30.  A problem with B*H*N == 0 is a successful no-op.
  *  - scale is the softmax scale s in S = s * Q K^T (the _ex forms take it;
  *    the others use 1/sqrt(d)).  dQ and dK include the factor s, dV does not.
  *  - Calls are asynchronous on the given HIP stream (hipStream_t passed as

@@ -134,6 +134,8 @@ int check_shape(int B, int H, int N, int d) {
   if (d != 64 && d != 128 && d != 256) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64, 128 or 256");
   if ((double)N * d * 4 >= 2147483648.0) return fail(DASH_ERR_INVALID_ARG, "N*d too large (per-head fp32 > 2 GiB)");
   if ((double)B * H >= 2147483647.0 / 1024) return fail(DASH_ERR_INVALID_ARG, "B*H too large");
+  // L and D of all rows are addressed with 32-bit byte offsets (4 bytes per row)
+  if ((double)B * H * N >= 1073741824.0) return fail(DASH_ERR_INVALID_ARG, "B*H*N too large (at most 2^30 - 1 rows)");
   return DASH_OK;
 }
 

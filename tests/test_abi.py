@@ -39,6 +39,7 @@ def test_argument_errors_without_device():
     assert call_bwd(lib, 0) == b.DASH_ERR_INVALID_ARG  # null pointers
     assert call_bwd(lib, 4096, d=96) == b.DASH_ERR_INVALID_ARG
     assert call_bwd(lib, 4096, N=-1) == b.DASH_ERR_INVALID_ARG
+    assert call_bwd(lib, 4096, B=1 << 14, H=1 << 6, N=1 << 10) == b.DASH_ERR_INVALID_ARG  # 2^30 rows
     assert call_bwd(lib, 4096, sched=9) == b.DASH_ERR_INVALID_ARG
     assert call_bwd(lib, 4096, sched=b.DASH_SCHED_SYMSHIFT, causal=0) == b.DASH_ERR_UNSUPPORTED
     assert "symmetric shift" in b.dash_last_error()
