@@ -276,11 +276,15 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       return st;
     };
     // Q / dO / L / D of block pb into LDS buffer b (asynchronous, vmcnt)
+    // Part k of a block is rows 16k (D = 128; 32k at D = 64) further down, i.e.
+    // 4 KB further in both the global tile and the LDS tile, with the same
+    // swizzle (tile_swz repeats every 16 / 32 rows).
+    static_assert((NT / CPR) * D * 2 == 4096 && NT * 16 == 4096, "a part is 4 KB");
     auto load_part = [&](int pb, int b, int k) {  // part k < QLD of the Q and dO rows
-      const int slot = k * NT + tid, r = slot / CPR, c = (slot % CPR) ^ tile_swz<D>(r);
+      const int r = tid / CPR, c = (tid % CPR) ^ tile_swz<D>(r);
       const uint32_t off = (uint32_t)((pb * BM + r) * D + 8 * c) * 2;
-      dma16(rq, lds_of(&sm.qs[b][(k * NT + 64 * w) * 8]), off);
-      dma16(rdo, lds_of(&sm.dos[b][(k * NT + 64 * w) * 8]), off);
+      const uint32_t at = lds_of(&sm.qs[b][64 * w * 8]) + 4096u * k;
+      dma16_pair(rq, rdo, at, at + (uint32_t)sizeof(sm.qs), off, 4096u * k);
     };
     auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
       const uint32_t row = (uint32_t)(bh * N + pb * BM + fresh_lane());  // < 2^30 (checked by the library)
@@ -304,13 +308,13 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     // device-coherent under XCD-local placement too: the atomic adds are
     // performed past the L2, so an L2 read of a counter can stay stale.
     auto poll_copy = [&](int pb) { dma4_coherent(rctr, lds_of(&sm.poll[w][0]), (uint32_t)pb * kCtrStride * 4); };
-    auto acc_copy = [&](int pb, int k) {  // chunk k of the slice into its landing pad
-      if constexpr (xcd) dma16_l2(racc, lds_of(&acc_w[k * 256]), acc_off(pb, 0), (uint32_t)k * 1024);
-      else dma16_coherent(racc, lds_of(&acc_w[k * 256]), acc_off(pb, 0), (uint32_t)k * 1024);
+    auto acc_copy = [&](int pb, int k4) {  // chunks 4 k4 .. 4 k4 + 3 of the slice into its landing pad
+      if constexpr (xcd) dma16x4_l2(racc, lds_of(&acc_w[k4 * 1024]), acc_off(pb, 0), 4096u * k4);
+      else dma16x4_coherent(racc, lds_of(&acc_w[k4 * 1024]), acc_off(pb, 0), 4096u * k4);
     };
     auto load_acc = [&](int pb) {
 #pragma unroll
-      for (int k = 0; k < NACC; ++k) acc_copy(pb, k);
+      for (int k4 = 0; k4 < NACC / 4; ++k4) acc_copy(pb, k4);
     };
     auto store_dkdv = [&](int j) {
       const auto rdk = make_rsrc((__bf16*)a.dk + head, hbytes);
@@ -543,7 +547,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int p = ks * 8 / KS; p < (ks + 1) * 8 / KS; ++p) {
           softmax_piece(0, p);
-          if (early_acc && p < NACC) acc_copy(pb, p);
+          if (early_acc && (p & 3) == 0 && p < NACC) acc_copy(pb, p >> 2);
         }
       });
       // run 3: dV/dK of half 0, with softmax of half 1

@@ -86,6 +86,31 @@ __device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc0 lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");
 }
+// Runs of copies sharing one m0.  The instruction offset field moves both
+// the global address and the LDS target, so four 1 KB copies at +0, +1 KB,
+// +2 KB and +3 KB of both take one m0 value (x4 forms).  A Q chunk and the
+// dO chunk at the same offset go to two LDS targets (pair form).
+#define DASH_DMA16X4(name, bits)                                                                  \
+  __device__ inline void name(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off, uint32_t soff) { \
+    uint32_t save;                                                                                \
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\t"                                     \
+                 "buffer_load_dwordx4 %2, %3, %4 offen " bits " lds\n\t"                          \
+                 "buffer_load_dwordx4 %2, %3, %4 offen offset:1024 " bits " lds\n\t"              \
+                 "buffer_load_dwordx4 %2, %3, %4 offen offset:2048 " bits " lds\n\t"              \
+                 "buffer_load_dwordx4 %2, %3, %4 offen offset:3072 " bits " lds\n\t"              \
+                 "s_mov_b32 m0, %0"                                                               \
+                 : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");               \
+  }
+DASH_DMA16X4(dma16x4_coherent, "sc1")
+DASH_DMA16X4(dma16x4_l2, "sc0")
+#undef DASH_DMA16X4
+__device__ inline void dma16_pair(__amdgpu_buffer_rsrc_t r0, __amdgpu_buffer_rsrc_t r1, uint32_t lds0, uint32_t lds1,
+                                  uint32_t off, uint32_t soff) {
+  uint32_t save;
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %3, %4, %6 offen lds\n\t"
+               "s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %3, %5, %6 offen lds\n\ts_mov_b32 m0, %0"
+               : "=&s"(save) : "s"(lds0), "s"(lds1), "v"(off), "s"(r0), "s"(r1), "s"(soff) : "memory");
+}
 __device__ inline void dma4(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off) {
   uint32_t save;
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
@@ -129,12 +154,10 @@ __device__ inline void vm_wait() {
 // operations of a wave complete in issue order, so this guarantees that
 // everything issued before the last n of them has completed.
 __device__ inline void vm_wait_le(int n) {
-  if (n >= 24) vm_wait<24>();
-  else if (n >= 17) vm_wait<17>();
-  else if (n >= 16) vm_wait<16>();
-  else if (n >= 9) vm_wait<9>();
+  // three levels: the common counts of the callers are 16-17 (a step's
+  // prefetch and accumulator copies or stores); the rare others wait longer
+  if (n >= 16) vm_wait<16>();
   else if (n >= 8) vm_wait<8>();
-  else if (n >= 1) vm_wait<1>();
   else vm_wait<0>();
 }
 
