@@ -138,17 +138,15 @@ typedef struct {
 #define DASH_TICKETS_CHAIN_MAJOR 2
 
 /* Placement of the work of a head.
-   XCD: every chain of head bh runs on XCD (die) bh % n_xcd, whose L2 then
-   holds that head's dQ accumulator and counters -- no other XCD touches them,
-   so the accumulator is read and written through the L2 instead of the
-   device-coherent path.  Each XCD takes work from its own ticket queue; a
-   Shift group is then at most 32 chains (what one XCD keeps resident), and a
-   head's groups run one after another.  Ordered schedules (naive, Descending,
-   Shift, Symmetric Shift), when the chains that must run at once fit one XCD
-   (Symmetric Shift: T_c <= 64).
+   XCD: every chain of head bh runs on XCD (die) bh % n_xcd; each XCD takes
+   work from its own ticket queue.  A Shift group is then at most 32 chains
+   (what one XCD keeps resident), and a head's groups run one after another.
+   The dQ accumulator is read and written device-coherently as under GLOBAL.
+   Ordered schedules (naive, Descending, Shift, Symmetric Shift), when the
+   chains that must run at once fit one XCD (Symmetric Shift: T_c <= 64);
+   else DASH_ERR_UNSUPPORTED.
    GLOBAL: one ticket queue for the whole GPU (any schedule, any d).
-   AUTO: XCD when it is possible, B*H is at least the number of XCDs and (for
-   Shift) T_c <= 256, else GLOBAL (dash_bwd_placement tells which). */
+   AUTO: GLOBAL (dash_bwd_placement reports it). */
 #define DASH_PLACEMENT_AUTO 0
 #define DASH_PLACEMENT_GLOBAL 1
 #define DASH_PLACEMENT_XCD 2

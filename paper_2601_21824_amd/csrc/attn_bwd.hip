@@ -214,8 +214,10 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   constexpr bool ordered = MODE == kModeOrdered || MODE == kModeOrderedXcd;
   // XCD-local placement: this workgroup serves the heads of its own XCD from
-  // that XCD's ticket queue, and the accumulator is read and written through
-  // the XCD's L2 (no other XCD touches those heads)
+  // that XCD's ticket queue (no other XCD touches those heads).  The
+  // accumulator is still read and written device-coherently (SC1), as under
+  // global placement: an L2-scope (SC0) read may hit this CU's L1, which keeps
+  // lines that workgroups on other CUs have since overwritten in the L2.
   constexpr bool xcd = MODE == kModeOrderedXcd;
   const int xq = xcd ? xcc_id() : 0;
   const int total = xcd ? (xq < a.nxcd ? xcd_heads(a.bh, a.nxcd, xq) * G.chains : 0) : a.bh * G.chains;
@@ -309,8 +311,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     // performed past the L2, so an L2 read of a counter can stay stale.
     auto poll_copy = [&](int pb) { dma4_coherent(rctr, lds_of(&sm.poll[w][0]), (uint32_t)pb * kCtrStride * 4); };
     auto acc_copy = [&](int pb, int k4) {  // chunks 4 k4 .. 4 k4 + 3 of the slice into its landing pad
-      if constexpr (xcd) dma16x4_l2(racc, lds_of(&acc_w[k4 * 1024]), acc_off(pb, 0), 4096u * k4);
-      else dma16x4_coherent(racc, lds_of(&acc_w[k4 * 1024]), acc_off(pb, 0), 4096u * k4);
+      dma16x4_coherent(racc, lds_of(&acc_w[k4 * 1024]), acc_off(pb, 0), 4096u * k4);
     };
     auto load_acc = [&](int pb) {
 #pragma unroll
@@ -662,8 +663,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
                 st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
                 if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
               } else {
-                if constexpr (xcd) st16(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
-                else st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
+                st16_coherent(racc, acc_off(pb, k), __builtin_bit_cast(u32x4, v));
               }
             }
           };

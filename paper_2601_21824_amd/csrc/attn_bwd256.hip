@@ -69,7 +69,8 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   const uint32_t hbytes = (uint32_t)((size_t)N * D * 2);
   constexpr bool ordered = ORDERED;  // false: the atomic variant
   // XCD-local placement (ordered only): the heads of this XCD from its own
-  // ticket queue, the accumulator through the XCD's L2
+  // ticket queue; the accumulator stays device-coherent (SC1) as under global
+  // placement, since an SC0 read may hit a stale line in this CU's L1
   constexpr bool xcd = XCD;
   const int xq = xcd ? xcc_id() : 0;
   const int total = xcd ? (xq < a.nxcd ? xcd_heads(a.bh, a.nxcd, xq) * G.chains : 0) : a.bh * G.chains;
@@ -141,8 +142,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
     auto load_acc = [&](int pb) {
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        if constexpr (xcd) lds_load16_l2(racc, &acc_w[t * 256], acc_off(pb, t));
-        else lds_load16_coherent(racc, &acc_w[t * 256], acc_off(pb, t));
+        lds_load16_coherent(racc, &acc_w[t * 256], acc_off(pb, t));
       }
     };
     auto store_dkdv = [&](int j) {
@@ -391,8 +391,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
               st8(rdq, off * 2, u32x2{pack_bf16(v[0] * a.scale, v[1] * a.scale), pack_bf16(v[2] * a.scale, v[3] * a.scale)});
               if (a.dq_accum) st16(make_rsrc(a.dq_accum + head, hbytes * 2), off * 4, __builtin_bit_cast(u32x4, v));
             } else {
-              if constexpr (xcd) st16(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
-              else st16_coherent(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
+              st16_coherent(racc, acc_off(pb, t), __builtin_bit_cast(u32x4, v));
             }
           }
         }

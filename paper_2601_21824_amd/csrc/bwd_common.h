@@ -45,9 +45,6 @@ __device__ inline void lds_load16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t 
 __device__ inline void lds_load16_coherent(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, kCoherent);
 }
-__device__ inline void lds_load16_l2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {  // SC0: the XCD's L2
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 16, off, 0, 0, 1);
-}
 __device__ inline void lds_load4(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)dst, 4, off, 0, 0, 0);
 }
@@ -79,13 +76,6 @@ __device__ inline void dma16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t lds, ui
   asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc1 lds\n\ts_mov_b32 m0, %0"
                : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");
 }
-// ... L2-coherent (SC0: the copy skips the CU's L1 and reads the XCD's L2),
-// for data that only workgroups of one XCD write and read
-__device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t off, uint32_t soff) {
-  uint32_t save;
-  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen sc0 lds\n\ts_mov_b32 m0, %0"
-               : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");
-}
 // Runs of copies sharing one m0.  The instruction offset field moves both
 // the global address and the LDS target, so four 1 KB copies at +0, +1 KB,
 // +2 KB and +3 KB of both take one m0 value (x4 forms).  A Q chunk and the
@@ -102,7 +92,6 @@ __device__ inline void dma16_l2(__amdgpu_buffer_rsrc_t r, uint32_t lds, uint32_t
                  : "=&s"(save) : "s"(lds), "v"(off), "s"(r), "s"(soff) : "memory");               \
   }
 DASH_DMA16X4(dma16x4_coherent, "sc1")
-DASH_DMA16X4(dma16x4_l2, "sc0")
 #undef DASH_DMA16X4
 __device__ inline void dma16_pair(__amdgpu_buffer_rsrc_t r0, __amdgpu_buffer_rsrc_t r1, uint32_t lds0, uint32_t lds1,
                                   uint32_t off, uint32_t soff) {

@@ -184,28 +184,23 @@ int occupancy(const DeviceInfo& di, int d) { return d == 64 ? di.occ64 : d == 12
 // a caller's workgroup cap leaves every XCD those chains -- except that a cap
 // never changes the summation order: where the placement decides Shift's
 // groups, a cap too small for XCD placement is rejected instead.
-int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, long heads, int want, int max_wg,
-                     bool* xcd) {
+int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, int want, bool* xcd) {
+  *xcd = false;
+  if (want != DASH_PLACEMENT_XCD) return DASH_OK;
+  // Automatic placement is global: with the accumulator read and written
+  // device-coherently under both placements, XCD-local placement measured
+  // within 2% of global at d = 64 and 128 under both masks (either way), and
+  // it caps a Shift group at the chains one XCD keeps resident.
   const bool ordered = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING || sched == DASH_SCHED_SHIFT ||
                        sched == DASH_SCHED_SYMSHIFT;
   dash::Geom Gx = dash::make_geom(sched, causal, N, d);
   dash::place_on_xcds(Gx);
   const long per_xcd = di.nxcd > 0 ? (long)occupancy(di, d) * di.cus / di.nxcd : 0;
   const long together = sched == DASH_SCHED_SHIFT ? Gx.grp : sched == DASH_SCHED_SYMSHIFT ? Gx.chains : 1;
-  const bool possible = di.nxcd > 0 && ordered && together <= per_xcd;
-  const bool order_depends = sched == DASH_SCHED_SHIFT && Gx.chains > dash::kXcdGroup;
-  const bool fits_cap = max_wg <= 0 || max_wg >= together * di.nxcd;
-  if (want == DASH_PLACEMENT_XCD) {
-    if (!possible)
-      return fail(DASH_ERR_UNSUPPORTED, "XCD-local placement needs an ordered schedule and the co-running chains "
-                                        "within one XCD's resident workgroups");
-    *xcd = true;
-  } else {
-    // measured: XCD placement is as fast or faster everywhere except Shift
-    // heads of more than 8 groups (d = 256, N = 32768: 7% slower)
-    const bool worth = !(sched == DASH_SCHED_SHIFT && Gx.t_c > 8 * dash::kXcdGroup);
-    *xcd = want == DASH_PLACEMENT_AUTO && possible && worth && heads >= di.nxcd && (fits_cap || order_depends);
-  }
+  if (!(di.nxcd > 0 && ordered && together <= per_xcd))
+    return fail(DASH_ERR_UNSUPPORTED, "XCD-local placement needs an ordered schedule and the co-running chains "
+                                      "within one XCD's resident workgroups");
+  *xcd = true;
   return DASH_OK;
 }
 
@@ -275,7 +270,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
 
   dash::Geom G = dash::make_geom(sched, causal, N, d);
   bool xcd = false;
-  if ((rc = choose_placement(di, sched, causal, N, d, (long)B * H, placement, opts ? opts->max_workgroups : 0, &xcd)))
+  if ((rc = choose_placement(di, sched, causal, N, d, placement, &xcd)))
     return rc;
   if (xcd) dash::place_on_xcds(G);
   const int nq = xcd ? di.nxcd : 1;  // ticket queues; workgroup i serves queue i % nq
@@ -295,10 +290,9 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
     // Q / dO and wins.  (Measured over d = 64 / 128 / 256 and both masks.)
     // Under XCD-local placement an XCD's queue holds several heads whose
     // chains outnumber its resident workgroups: chain-major keeps the naive
-    // pipeline fill short there as well (B=2 N=8192: +7% full, +25% causal),
-    // and for Descending except with a causal mask at d = 128, where its
-    // chains all start at the last Q tile and head-major measured 6% better
-    // (at d = 64 chain-major is 6% better).
+    // pipeline fill short there as well, and for Descending except with a
+    // causal mask at d = 128, where its chains all start at the last Q tile
+    // and head-major measured better.
     const bool waits = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING;
     if (xcd)
       G.chain_major = sched == DASH_SCHED_NAIVE || (sched == DASH_SCHED_DESCENDING && (!causal || d < 128));
@@ -407,7 +401,7 @@ int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule) {
   DeviceInfo di;
   if ((rc = device_info(&di))) return rc;
   bool xcd = false;
-  if ((rc = choose_placement(di, resolve(schedule, d, causal), causal, N, d, (long)B * H, DASH_PLACEMENT_AUTO, 0, &xcd)))
+  if ((rc = choose_placement(di, resolve(schedule, d, causal), causal, N, d, DASH_PLACEMENT_AUTO, &xcd)))
     return rc;
   return xcd ? DASH_PLACEMENT_XCD : DASH_PLACEMENT_GLOBAL;
 }

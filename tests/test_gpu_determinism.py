@@ -13,7 +13,7 @@ from paper_2601_21824_amd import binding as dash
 
 pytestmark = pytest.mark.gpu
 
-DET_CASES = [
+DET_CASES = [  # (B, H, N, d, causal, schedule[, placement])
     (4, 16, 1024, 64, True, "naive"),
     (4, 16, 1024, 64, True, "descending"),
     (4, 16, 1024, 64, True, "symshift"),
@@ -26,20 +26,27 @@ DET_CASES = [
     (1, 2, 1024, 256, True, "symshift"),
     (2, 4, 2048, 128, True, "split"),
     (2, 4, 2048, 128, False, "partials"),
+    # XCD-local placement: several workgroups of one head on each XCD read
+    # the accumulator slots that the others wrote just before
+    (4, 16, 1024, 64, True, "descending", 2),
+    (2, 8, 2048, 128, False, "shift", 2),
+    (2, 8, 1024, 256, True, "naive", 2),
 ]
 
 
-@pytest.mark.parametrize("case", DET_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in DET_CASES])
+@pytest.mark.parametrize("case", DET_CASES, ids=[f"N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}{'-xcd' if c[6:] == (2,) else ''}"
+                                                 for c in DET_CASES])
 def test_bitwise_identical_over_100_runs(case):
-    B, H, N, d, causal, sched = case
+    B, H, N, d, causal, sched = case[:6]
+    opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 0, 0, case[6]) if len(case) > 6 else None
     print(f"\n[determinism] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=77)
     og, lseg = run_fwd(qg, kg, vg, causal)
     ws = dash.new_workspace(B, H, N, d, sched)
-    first = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
+    first = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts)
     outs = [torch.empty_like(t) for t in first]
     for r in range(99):
-        dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, *outs, causal, sched, workspace=ws)
+        dash.dash_attn_bwd(qg, kg, vg, og, dog, lseg, *outs, causal, sched, workspace=ws, options=opts)
         torch.cuda.synchronize()
         for a, b in zip(first, outs):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"run {r + 2} differs"
@@ -257,27 +264,25 @@ PLACE_CASES = [
 @pytest.mark.parametrize("case", PLACE_CASES, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}"
                                                     for c in PLACE_CASES])
 def test_placement(case):
-    """XCD-local placement (each head's chains and accumulator on one XCD)
-    against one global queue: bitwise the same result wherever the schedule's
-    order does not depend on the placement (all but Shift with more than 32
-    KV tiles, whose groups shrink to 32 chains); there the witnessed order is
-    the oracle's with groups of 32, and the result is deterministic.
-    AUTO takes XCD placement for B*H >= the XCD count, and a workgroup cap
-    below one XCD's co-running chains per XCD falls back to the global queue
-    where that leaves the bits unchanged."""
+    """XCD-local placement (each head's chains on one XCD, from that XCD's
+    ticket queue) against one global queue: bitwise the same result wherever
+    the schedule's order does not depend on the placement (all but Shift with
+    more than 32 KV tiles, whose groups shrink to 32 chains); there the
+    witnessed order is the oracle's with groups of 32, and the result is
+    deterministic.  AUTO is the global queue, also under a workgroup cap."""
     B, H, N, d, causal, sched = case
     print(f"\n[placement] {case}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=23)
     og, lseg = run_fwd(qg, kg, vg, causal)
     ws = dash.new_workspace(B, H, N, d, sched)
-    assert dash.dash_bwd_placement(B, H, N, d, causal, sched) == XL
+    assert dash.dash_bwd_placement(B, H, N, d, causal, sched) == GL
     place = lambda p, cap=0: dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap, 0, p)
     auto = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws)
     assert dash.dash_bwd_check(ws) == dash.DASH_OK
     xcd = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(XL))
     glob = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=place(GL))
     assert dash.dash_bwd_check(ws) == dash.DASH_OK
-    for a_, b_ in zip(auto, xcd):
+    for a_, b_ in zip(auto, glob):
         assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
     tab_x = dash.dash_schedule_table(sched, N, d, causal, XL)
     tab_g = dash.dash_schedule_table(sched, N, d, causal, GL)
