@@ -77,6 +77,25 @@ def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
     return wall * 1e3 / steps, sum(main_ms) / len(main_ms)
 
 
+def ordering_wait(dash, tensors, causal, sched, B, H, N, d):
+    """One instrumented (untimed) call: the share of the main kernel's
+    wave-time spent waiting for a dQ turn, and the share of wave-steps whose
+    turn was not yet visible one step ahead (those waited)."""
+    import torch
+    q, k, v, o, do, lse, dq, dk, dv, ws = tensors
+    stats = torch.zeros(3, dtype=torch.int64, device=q.device)
+    opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 0, 0, 0, stats.data_ptr())
+    dash.dash_attn_bwd(q, k, v, o, do, lse, dq, dk, dv, causal, sched, workspace=ws, options=opts)
+    if dash.dash_bwd_check(ws) != dash.DASH_OK:
+        raise RuntimeError(f"{sched}: ordering wait timed out (instrumented call)")
+    late, wait_ticks, wave_ticks = (int(x) for x in stats.cpu())
+    tab = dash.dash_schedule_table(sched, N, d, causal)
+    wave_steps = 4 * B * H * int(tab["chain_len"].sum()) * (tab["br"] // 64)  # 64-row steps, 4 waves
+    return {"stall_frac": round(wait_ticks / wave_ticks, 4) if wave_ticks > 0 else None,
+            "late_wave_steps": late, "wave_steps": wave_steps,
+            "late_frac": round(late / wave_steps, 4) if wave_steps else None}
+
+
 def measured_traffic():
     """HBM bytes per launch of the main kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, or None if the kernel source changed since
@@ -243,6 +262,9 @@ def main():
                      "traffic": measured_traffic() if (N, d, causal, det) == (8192, 128, False, "shift") else None,
                      "main_kernel_ms": round(main_ms, 4)},
     }
+    # the ordering wait, measured in an extra instrumented call per ordered schedule
+    out["ordering_wait"] = {s_: ordering_wait(dash, tensors, causal, s_, B, H, N, d)
+                            for s_ in results if s_ not in ("atomic", "split", "partials")}
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(q, k, v, do, causal, flops / (B * H))
     print(json.dumps(out), flush=True)

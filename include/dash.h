@@ -131,6 +131,16 @@ typedef struct {
      of dash_schedule_table) when a head has more than 32 KV tiles; no other
      schedule's. */
   int placement;
+  /* If non-NULL: device memory, 3 uint64 counters that the call adds to
+     (zero them first).  Ordering-wait statistics of the main kernel:
+     [0] wave-steps whose turn was not yet visible when the wave first looked
+         (one step ahead) and that waited for it at the end of the step;
+     [1] real-time clock ticks those waits took;
+     [2] ticks of every wave's run, from its start to its exit.
+     [1] / [2] is the share of wave time spent in the ordering wait.  The
+     atomic and comparison variants add to [2] only.  Instrumented calls add
+     a few atomics per wave; the results are the same bits. */
+  unsigned long long* wait_stats;
 } dash_bwd_options_t;
 
 #define DASH_TICKETS_AUTO 0

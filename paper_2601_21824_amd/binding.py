@@ -43,7 +43,8 @@ class dash_bwd_options_t(ctypes.Structure):
                 ("witness", ctypes.c_void_p), ("partials", ctypes.c_void_p),
                 ("dq_accum", ctypes.c_void_p), ("event_main_begin", ctypes.c_void_p),
                 ("event_main_end", ctypes.c_void_p), ("max_workgroups", ctypes.c_int),
-                ("ticket_order", ctypes.c_int), ("placement", ctypes.c_int)]
+                ("ticket_order", ctypes.c_int), ("placement", ctypes.c_int),
+                ("wait_stats", ctypes.c_void_p)]
 
 
 _lib = None

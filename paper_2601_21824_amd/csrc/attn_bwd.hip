@@ -185,7 +185,7 @@ struct MainSmem {
   int item;
 };
 
-template <int D, bool CAUSAL, int MODE>
+template <int D, bool CAUSAL, int MODE, bool STATS = false>
 __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   constexpr int BC = kTileKV;   // KV rows per tile (128 for d = 64 and 128)
   constexpr int NW = BC / 32;   // waves, 32 KV rows each
@@ -235,6 +235,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   // step's barrier, by which time the accumulator stores have drained.
   const bool deferred = G.sched == S_SHIFT || G.sched == S_SYMSHIFT;
   bool failed = false;  // this wave hit a wait timeout: skip further waits
+  if constexpr (STATS) stats_wave_begin(a.wait_stats, l);
 
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(ticket, 1);
@@ -623,7 +624,10 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         bool add = false;  // accumulate into the slice (else: the partial is stored as is)
         if (ordered) {
           if (!have_turn && !failed) {
+            if constexpr (STATS) vm_wait<0>();  // time the wait only, not this wave's own loads
+            const unsigned long long t0 = STATS ? clock_now() : 0ull;
             have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
+            if constexpr (STATS) stats_wait(a.wait_stats, l, t0);
             if (!have_turn) {
               failed = true;
               __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -732,6 +736,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     if (cur_j >= 0) store_dkdv(cur_j);
     __syncthreads();  // sm.item is rewritten by the next ticket
   }
+  if constexpr (STATS) stats_wave_end(a.wait_stats, l);
 }
 
 template <int D, bool CAUSAL>
@@ -743,8 +748,12 @@ void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModePartials>), grid, block, 0, stream, a);
   else if (a.G.sched == S_SPLIT)
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeNoDq>), grid, block, 0, stream, a);
+  else if (a.nxcd > 0 && a.wait_stats)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrderedXcd, true>), grid, block, 0, stream, a);
   else if (a.nxcd > 0)
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrderedXcd>), grid, block, 0, stream, a);
+  else if (a.wait_stats)
+    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered, true>), grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered>), grid, block, 0, stream, a);
 }
@@ -792,12 +801,16 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 template <int D>
 int main_occupancy() {
   int lo = 1 << 30;
-  const void* fns[10] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
+  const void* fns[14] = {(const void*)bwd_main_kernel<D, false, kModeAtomic>, (const void*)bwd_main_kernel<D, false, kModeOrdered>,
                          (const void*)bwd_main_kernel<D, false, kModePartials>, (const void*)bwd_main_kernel<D, false, kModeNoDq>,
                          (const void*)bwd_main_kernel<D, false, kModeOrderedXcd>,
+                         (const void*)bwd_main_kernel<D, false, kModeOrdered, true>,
+                         (const void*)bwd_main_kernel<D, false, kModeOrderedXcd, true>,
                          (const void*)bwd_main_kernel<D, true, kModeAtomic>, (const void*)bwd_main_kernel<D, true, kModeOrdered>,
                          (const void*)bwd_main_kernel<D, true, kModePartials>, (const void*)bwd_main_kernel<D, true, kModeNoDq>,
-                         (const void*)bwd_main_kernel<D, true, kModeOrderedXcd>};
+                         (const void*)bwd_main_kernel<D, true, kModeOrderedXcd>,
+                         (const void*)bwd_main_kernel<D, true, kModeOrdered, true>,
+                         (const void*)bwd_main_kernel<D, true, kModeOrderedXcd, true>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, 256, 0) != hipSuccess) return 0;

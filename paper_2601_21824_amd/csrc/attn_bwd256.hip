@@ -57,7 +57,7 @@ struct Smem256 {
   int item;
 };
 
-template <bool CAUSAL, bool ORDERED, bool XCD>
+template <bool CAUSAL, bool ORDERED, bool XCD, bool STATS = false>
 __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) Smem256 sm;
 
@@ -81,6 +81,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   // step's dV/dK work has covered the store latency.
   const bool deferred = G.sched == S_SHIFT || G.sched == S_SYMSHIFT;
   bool failed = false;
+  if constexpr (STATS) stats_wave_begin(a.wait_stats, l);
 
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(ticket, 1);
@@ -360,7 +361,10 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
       bool add = false;
       if (ordered) {
         if (!have_turn && !failed) {
+          if constexpr (STATS) vm_wait<0>();  // time the wait only, not this wave's own loads
+          const unsigned long long t0 = STATS ? clock_now() : 0ull;
           have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
+          if constexpr (STATS) stats_wait(a.wait_stats, l, t0);
           if (!have_turn) {
             failed = true;
             __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -422,6 +426,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
     if (cur_j >= 0) store_dkdv(cur_j);
     __syncthreads();  // sm.item is rewritten by the next ticket
   }
+  if constexpr (STATS) stats_wave_end(a.wait_stats, l);
 }
 
 }  // namespace
@@ -431,20 +436,26 @@ void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream) {
   const dim3 grid(grid_main), block(NT);
   if (a.G.causal) {
     if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<true, false, false>), grid, block, 0, stream, a);
+    else if (a.nxcd > 0 && a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<true, true, true, true>), grid, block, 0, stream, a);
     else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<true, true, true>), grid, block, 0, stream, a);
+    else if (a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<true, true, false, true>), grid, block, 0, stream, a);
     else hipLaunchKernelGGL((bwd_main256_kernel<true, true, false>), grid, block, 0, stream, a);
   } else {
     if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<false, false, false>), grid, block, 0, stream, a);
+    else if (a.nxcd > 0 && a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<false, true, true, true>), grid, block, 0, stream, a);
     else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<false, true, true>), grid, block, 0, stream, a);
+    else if (a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<false, true, false, true>), grid, block, 0, stream, a);
     else hipLaunchKernelGGL((bwd_main256_kernel<false, true, false>), grid, block, 0, stream, a);
   }
 }
 
 int bwd_main256_occupancy() {
   int lo = 1 << 30;
-  const void* fns[6] = {(const void*)bwd_main256_kernel<false, false, false>, (const void*)bwd_main256_kernel<false, true, false>,
-                        (const void*)bwd_main256_kernel<false, true, true>, (const void*)bwd_main256_kernel<true, false, false>,
-                        (const void*)bwd_main256_kernel<true, true, false>, (const void*)bwd_main256_kernel<true, true, true>};
+  const void* fns[10] = {(const void*)bwd_main256_kernel<false, false, false>, (const void*)bwd_main256_kernel<false, true, false>,
+                         (const void*)bwd_main256_kernel<false, true, true>, (const void*)bwd_main256_kernel<true, false, false>,
+                         (const void*)bwd_main256_kernel<true, true, false>, (const void*)bwd_main256_kernel<true, true, true>,
+                         (const void*)bwd_main256_kernel<false, true, false, true>, (const void*)bwd_main256_kernel<false, true, true, true>,
+                         (const void*)bwd_main256_kernel<true, true, false, true>, (const void*)bwd_main256_kernel<true, true, true, true>};
   for (const void* f : fns) {
     int blocks = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, f, NT, 0) != hipSuccess) return 0;

@@ -27,6 +27,24 @@ __device__ inline bool wait_turn(const int* ctr, int want, int limit) {
   return true;
 }
 
+// Ordering-wait statistics (instrumented kernels only): lane 0 of each wave
+// subtracts its start time from st[2] and adds its exit time, and adds one to
+// st[0] and the ticks it spent to st[1] for every wait at the end of a step
+// (the turn was not visible at the early look).  Real-time clock ticks.
+__device__ inline unsigned long long clock_now() { return (unsigned long long)__builtin_amdgcn_s_memrealtime(); }
+__device__ inline void stats_wave_begin(unsigned long long* st, int lane) {
+  if (lane == 0) atomicAdd(&st[2], 0ull - clock_now());
+}
+__device__ inline void stats_wave_end(unsigned long long* st, int lane) {
+  if (lane == 0) atomicAdd(&st[2], clock_now());
+}
+__device__ inline void stats_wait(unsigned long long* st, int lane, unsigned long long t0) {
+  if (lane == 0) {
+    atomicAdd(&st[0], 1ull);
+    atomicAdd(&st[1], clock_now() - t0);
+  }
+}
+
 // 4 bf16 of one column from 4 consecutive rows (gfx950 transpose read): within
 // each group of 16 lanes, lane L addresses row L/4, columns 4*(L%4)..+3 of a
 // 4 x 16 tile and receives column L of it.

@@ -342,6 +342,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   a.nxcd = xcd ? di.nxcd : 0;
   a.xcd_cap = xcd_cap;
   a.witness = opts ? opts->witness : nullptr;
+  a.wait_stats = opts ? opts->wait_stats : nullptr;
   a.partials = opts ? opts->partials : nullptr;
   a.dq_accum = opts ? opts->dq_accum : nullptr;
   a.bh = B * H;

@@ -63,6 +63,7 @@ struct BwdArgs {
   int poison;
   Geom G;
   hipEvent_t ev_begin, ev_end;  // optional, recorded around bwd_main
+  unsigned long long* wait_stats;  // optional ordering-wait statistics (see dash_bwd_options_t)
 };
 
 hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream);
