@@ -31,7 +31,7 @@ constexpr int kModeAtomic = 0;    // fp32 atomic adds into dQacc (non-determinis
 constexpr int kModeOrdered = 1;   // the ordered reduction (every DASH schedule)
 constexpr int kModePartials = 2;  // store it in its own buffer; bwd_sum_partials adds them in KV order
 constexpr int kModeNoDq = 3;      // no dQ at all: dK, dV only (SPLIT's first pass)
-constexpr int kModeOrderedXcd = 4;  // the ordered reduction with every head on one XCD (L2-local accumulator)
+constexpr int kModeOrderedXcd = 4;  // the ordered reduction with every chain of a head on one XCD
 
 struct BwdArgs {
   const void* q;

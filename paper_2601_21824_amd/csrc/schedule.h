@@ -141,9 +141,8 @@ DASH_HD void task(const Geom& G, int w, int t, int* j, int* i) {
   }
 }
 
-// XCD-local placement: every chain of head bh runs on XCD bh % nxcd, so the
-// head's dQ accumulator and counters stay in that XCD's L2.  A Shift group
-// must then fit one XCD's resident workgroups: groups of at most kXcdGroup
+// XCD-local placement: every chain of head bh runs on XCD bh % nxcd, from
+// that XCD's own ticket queue.  A Shift group must then fit one XCD's resident workgroups: groups of at most kXcdGroup
 // chains, which the XCD runs one after another (the group-major order of
 // rank_of).  The other schedules' orders do not depend on the placement.
 DASH_HD void place_on_xcds(Geom& G) {

@@ -122,7 +122,7 @@ PROTO_CASES = [
     (1, 2, 512, 256, False, "shift", GL),
     (1, 2, 512, 256, True, "symshift", GL),
     (1, 1, 333, 256, True, "descending", GL),
-    # every chain of a head on one XCD (L2-local accumulator); at 33 KV tiles
+    # every chain of a head on one XCD; at 33 KV tiles
     # Shift runs as two groups, 32 chains then 1
     (1, 2, 4224, 128, False, "shift", XL),
     (3, 3, 700, 64, False, "shift", XL),
