@@ -262,6 +262,10 @@ def main():
                      "traffic": measured_traffic() if (N, d, causal, det) == (8192, 128, False, "shift") else None,
                      "main_kernel_ms": round(main_ms, 4)},
     }
+    # the measured MFMA peak of this device beside the published one
+    measured = dash.dash_mfma_peak()
+    out["roofline"]["measured_peak"] = round(measured, 1)
+    out["roofline"]["frac_of_measured"] = round(main_tflops / measured, 4) if measured > 0 else None
     # the ordering wait, measured in an extra instrumented call per ordered schedule
     out["ordering_wait"] = {s_: ordering_wait(dash, tensors, causal, s_, B, H, N, d)
                             for s_ in results if s_ not in ("atomic", "split", "partials")}

@@ -215,6 +215,15 @@ int dash_resolve_schedule(int schedule, int d, int causal);
    device, or a negative dash_status_t.  Needs the device (queries it once). */
 int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule);
 
+/* Measured bf16 dense MFMA throughput of the current device, the measured
+   counterpart of the published 2.5 PFLOP/s in the main kernel's roofline.
+   Two workgroups of 4 waves per CU each run `iters` rounds of 8 independent
+   v_mfma_f32_32x32x16_bf16 chains on register operands (iters = 0: 20000,
+   about 4 ms); *tflops receives the best of 3 event-timed launches in
+   TFLOP/s.  Synchronous; allocates and frees a small device buffer and its
+   own stream.  DASH_ERR_INVALID_ARG for a NULL tflops or iters < 0. */
+int dash_mfma_peak(int iters, double* tflops);
+
 /*
  * Host-side view of the schedule the kernels follow (no GPU needed).  For one
  * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c

@@ -29,7 +29,7 @@ DASH_PLACEMENT_AUTO, DASH_PLACEMENT_GLOBAL, DASH_PLACEMENT_XCD = 0, 1, 2
 # every symbol include/dash.h declares
 EXPORTS = ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_bwd_workspace_size",
            "dash_attn_bwd_ex", "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table",
-           "dash_bwd_placement", "dash_last_error", "dash_release_workspace")
+           "dash_bwd_placement", "dash_mfma_peak", "dash_last_error", "dash_release_workspace")
 
 
 class DashError(RuntimeError):
@@ -70,10 +70,12 @@ def load():
         lib.dash_resolve_schedule.argtypes = [ci] * 3
         lib.dash_schedule_table.argtypes = [ci] * 5 + [ip] * 5
         lib.dash_bwd_placement.argtypes = [ci] * 6
+        lib.dash_mfma_peak.argtypes = [ci, ctypes.POINTER(ctypes.c_double)]
         lib.dash_last_error.restype = ctypes.c_char_p
         lib.dash_release_workspace.restype = None
         for f in ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_attn_bwd_ex",
-                  "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table", "dash_bwd_placement"):
+                  "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table", "dash_bwd_placement",
+                  "dash_mfma_peak"):
             getattr(lib, f).restype = ci
         _lib = lib
     return _lib
@@ -177,6 +179,13 @@ def dash_bwd_placement(B: int, H: int, N: int, d: int, causal: bool, schedule="a
     if rc < 0:
         _check(rc)
     return rc
+
+
+def dash_mfma_peak(iters: int = 0) -> float:
+    """Measured bf16 dense MFMA throughput of the current device in TFLOP/s."""
+    out = ctypes.c_double(0.0)
+    _check(load().dash_mfma_peak(int(iters), ctypes.byref(out)))
+    return out.value
 
 
 def dash_schedule_table(schedule, N: int, d: int, causal: bool, placement=DASH_PLACEMENT_GLOBAL) -> dict:

@@ -407,6 +407,44 @@ int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule) {
   return xcd ? DASH_PLACEMENT_XCD : DASH_PLACEMENT_GLOBAL;
 }
 
+int dash_mfma_peak(int iters, double* tflops) {
+  if (!tflops) return fail(DASH_ERR_INVALID_ARG, "tflops is NULL");
+  if (iters < 0) return fail(DASH_ERR_INVALID_ARG, "iters < 0");
+  if (iters == 0) iters = 20000;
+  DeviceInfo di;
+  int rc = device_info(&di);
+  if (rc) return rc;
+  const int grid = 2 * di.cus;  // two workgroups (8 waves) per CU
+  float* sink = nullptr;
+  hipError_t e = hipMalloc(&sink, (size_t)grid * 256 * sizeof(float));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+  hipStream_t st = nullptr;
+  hipEvent_t b = nullptr, en = nullptr;
+  double best = 0.0;
+  if ((e = hipStreamCreate(&st)) == hipSuccess && (e = hipEventCreate(&b)) == hipSuccess &&
+      (e = hipEventCreate(&en)) == hipSuccess) {
+    dash::launch_mfma_peak(grid, iters / 10 + 1, sink, st);  // warm-up (clocks up)
+    for (int rep = 0; rep < 3 && e == hipSuccess; ++rep) {
+      (void)hipEventRecord(b, st);
+      dash::launch_mfma_peak(grid, iters, sink, st);
+      (void)hipEventRecord(en, st);
+      if ((e = hipEventSynchronize(en)) != hipSuccess) break;
+      float ms = 0.f;
+      if ((e = hipEventElapsedTime(&ms, b, en)) != hipSuccess) break;
+      const double t = dash::mfma_peak_flops_per_launch(grid, iters) / (ms * 1e-3) / 1e12;
+      best = t > best ? t : best;
+    }
+    if (e == hipSuccess) e = hipGetLastError();
+  }
+  if (en) (void)hipEventDestroy(en);
+  if (b) (void)hipEventDestroy(b);
+  if (st) (void)hipStreamDestroy(st);
+  (void)hipFree(sink);
+  if (e != hipSuccess) return hip_fail(e, "MFMA peak measurement");
+  *tflops = best;
+  return DASH_OK;
+}
+
 void dash_release_workspace(void) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   if (g_ws) (void)hipFree(g_ws);

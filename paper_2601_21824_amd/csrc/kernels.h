@@ -73,5 +73,8 @@ int bwd_main_occupancy(int d);
 // head dim 256 (attn_bwd256.hip)
 void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream);
 int bwd_main256_occupancy();
+// measured MFMA throughput (mfma_peak.hip): grid workgroups of 4 waves
+void launch_mfma_peak(int grid, int iters, float* sink, hipStream_t stream);
+double mfma_peak_flops_per_launch(int grid, int iters);
 
 }  // namespace dash

@@ -75,6 +75,10 @@ def test_argument_errors_without_device():
                               1 << 40, ctypes.byref(opts), None)
     assert rc == b.DASH_ERR_INVALID_ARG and "placement" in b.dash_last_error()
     assert lib.dash_schedule_table(1, 128, 64, 0, 0, None, None, None, None, None) == b.DASH_ERR_INVALID_ARG
+    # the MFMA peak measurement checks its arguments before touching the device
+    assert lib.dash_mfma_peak(0, None) == b.DASH_ERR_INVALID_ARG
+    out = ctypes.c_double(0.0)
+    assert lib.dash_mfma_peak(-1, ctypes.byref(out)) == b.DASH_ERR_INVALID_ARG
 
 
 def test_schedule_resolution():
