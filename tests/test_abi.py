@@ -131,3 +131,23 @@ def test_schedule_table_matches_oracle(sched, causal, N, d, placement):
     if kind in (osched.SHIFT, osched.SYMSHIFT):
         props = osched.check(ref, t_r, t_c, causal, br, bc, group=grp if kind == osched.SHIFT else None)
         assert props["coverage"] and props["conflict_free"] and props["monotone"]
+
+
+def test_missing_library_raises_instead_of_falling_back():
+    """With no built library the binding raises; nothing computes on the CPU."""
+    import subprocess
+    import sys
+    code = (
+        "import sys, torch\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "from paper_2601_21824_amd import binding as b\n"
+        "b.LIB_PATH = '/nonexistent/libdash.so'\n"
+        "q = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)\n"
+        "try:\n"
+        "    b.attn_bwd(q, q, q, q, q, torch.zeros(1, 1, 64), False, 'shift')\n"
+        "except b.DashError as e:\n"
+        "    print('raised', e.code, e)\n"
+        "    sys.exit(0)\n"
+        "sys.exit(1)\n")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "is not built" in r.stdout, r.stdout + r.stderr
