@@ -134,7 +134,8 @@ def test_schedule_table_matches_oracle(sched, causal, N, d, placement):
 
 
 def test_missing_library_raises_instead_of_falling_back():
-    """With no built library the binding raises; nothing computes on the CPU."""
+    """With no built library every entry point raises, and CPU tensors are
+    refused rather than computed on: there is no CPU fallback."""
     import subprocess
     import sys
     code = (
@@ -142,12 +143,19 @@ def test_missing_library_raises_instead_of_falling_back():
         f"sys.path.insert(0, {ROOT!r})\n"
         "from paper_2601_21824_amd import binding as b\n"
         "b.LIB_PATH = '/nonexistent/libdash.so'\n"
+        "for call in (b.load, lambda: b.dash_resolve_schedule('auto', 128, False),\n"
+        "             lambda: b.dash_bwd_workspace_size(1, 1, 64, 64)):\n"
+        "    try:\n"
+        "        call()\n"
+        "        sys.exit(1)\n"
+        "    except b.DashError as e:\n"
+        "        assert 'is not built' in str(e), e\n"
         "q = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)\n"
         "try:\n"
         "    b.attn_bwd(q, q, q, q, q, torch.zeros(1, 1, 64), False, 'shift')\n"
+        "    sys.exit(1)\n"
         "except b.DashError as e:\n"
-        "    print('raised', e.code, e)\n"
-        "    sys.exit(0)\n"
-        "sys.exit(1)\n")
+        "    assert 'device tensors' in str(e), e\n"
+        "print('ok')\n")
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
-    assert r.returncode == 0 and "is not built" in r.stdout, r.stdout + r.stderr
+    assert r.returncode == 0 and "ok" in r.stdout, r.stdout + r.stderr
