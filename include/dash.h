@@ -135,7 +135,8 @@ typedef struct {
      (zero them first).  Ordering-wait statistics of the main kernel:
      [0] wave-steps whose turn was not yet visible when the wave first looked
          (one step ahead) and that waited for it at the end of the step;
-     [1] real-time clock ticks those waits took;
+     [1] real-time clock ticks those waits took, counted from the moment the
+         wave's own outstanding loads have landed (polls and sleeps only);
      [2] ticks of every wave's run, from its start to its exit.
      [1] / [2] is the share of wave time spent in the ordering wait.  The
      atomic and comparison variants add to [2] only.  Instrumented calls add
