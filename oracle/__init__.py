@@ -108,12 +108,51 @@ def attn_fwd(q, k, v, causal: bool, scale=None, rows=None):
     return o.reshape(*lead, n, d), lse.reshape(*lead, n)
 
 
+def lse_and_d(q, k, v, do, causal: bool, scale=None, block=512):
+    """L and D of every query row of one head ([N, d] inputs), fp64.
+
+    The two row vectors the backward needs besides Q, K, V and dO (the
+    Background section's logsumexp vector L and Algorithm 1's preprocessing
+    D = rowsum(dO o O)), from their definitions, for query rows taken ``block``
+    at a time: S = scale * Q_b K^T (a library fp64 matrix product), masked
+    entries -inf, L = m + log sum exp(S - m) with m the row maximum,
+    P = exp(S - L), O_b = P V (a library product), D = sum over columns of
+    dO_b o O_b.  No blocking over keys, so each row's sums are the plain
+    definitions; it exists because the C row functions take minutes for
+    every row of a 32768-row head, which sampled dK/dV rows need.  With a
+    causal mask only the keys up to the block's last row enter, and P is
+    formed as exp(S - m) / sum exp(S - m), which equals exp(S - L).
+    """
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
+    n, d = q.shape
+    s = _scale(d, scale)
+    lse = np.empty(n)
+    dvec = np.empty(n)
+    for r0 in range(0, n, block):
+        r1 = min(n, r0 + block)
+        nk = r1 if causal else n  # keys past the block's last row are masked for all its rows
+        sc = s * (q[r0:r1] @ k[:nk].T)
+        if causal:  # query r0 + a sees key r0 + b iff b <= a
+            diag = sc[:, r0:r1]
+            diag[np.triu(np.ones((r1 - r0, r1 - r0), dtype=bool), 1)] = -np.inf
+        m = sc.max(axis=1, keepdims=True)
+        e = np.exp(sc - m)
+        z = e.sum(axis=1, keepdims=True)
+        lb = m + np.log(z)
+        ob = (e / z) @ v[:nk]
+        lse[r0:r1] = lb[:, 0]
+        dvec[r0:r1] = np.sum(do[r0:r1] * ob, axis=1)
+    return lse, dvec
+
+
 def attn_bwd(q, k, v, do, causal: bool, scale=None, dq_rows=None, kv_rows=None):
     """dQ, dK, dV (fp64) of attention, plus the L and D vectors used.
 
     ``dq_rows`` / ``kv_rows`` restrict which rows of dQ / dK,dV are produced
-    (others NaN).  Computing any dK/dV row needs L and D of every query row,
-    so those are always computed for all rows.
+    (others NaN).  Computing any dK/dV row needs L and D of every query row:
+    with every dQ row requested they come from the same row-by-row pass;
+    with only some dQ rows, from ``lse_and_d`` (all rows) while dQ is
+    computed for the requested rows only.
     """
     lib = _load()
     q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
@@ -126,21 +165,17 @@ def attn_bwd(q, k, v, do, causal: bool, scale=None, dq_rows=None, kv_rows=None):
     dv = np.full((heads, n, d), np.nan)
     lse = np.full((heads, n), np.nan)
     dvec = np.full((heads, n), np.nan)
-    all_rows = _rows(None, n)
     qr = _rows(dq_rows, n)
     kr = _rows(kv_rows, n)
     for h in range(heads):
         qh, kh, vh, doh = (np.ascontiguousarray(a[h]) for a in arrs)
         dqh = np.full((n, d), np.nan)
         lh, Dh = np.full(n, np.nan), np.full(n, np.nan)
-        need_all = len(kr) > 0
-        rows_for_dq = all_rows if need_all else qr
-        lib.oracle_bwd_dq_rows(_p(qh), _p(kh), _p(vh), _p(doh), n, d, int(causal), s,
-                               _ip(rows_for_dq), len(rows_for_dq), _p(dqh), _p(lh), _p(Dh))
-        if need_all and dq_rows is not None:
-            keep = np.full((n, d), np.nan)
-            keep[qr] = dqh[qr]
-            dqh = keep
+        if len(qr):
+            lib.oracle_bwd_dq_rows(_p(qh), _p(kh), _p(vh), _p(doh), n, d, int(causal), s,
+                                   _ip(qr), len(qr), _p(dqh), _p(lh), _p(Dh))
+        if len(kr) and dq_rows is not None:  # L and D of the rows dQ did not cover
+            lh, Dh = lse_and_d(qh, kh, vh, doh, causal, scale)
         dkh, dvh = np.full((n, d), np.nan), np.full((n, d), np.nan)
         if len(kr):
             lib.oracle_bwd_dkdv_cols(_p(qh), _p(kh), _p(vh), _p(doh), n, d, int(causal), s,
