@@ -139,8 +139,10 @@ typedef struct {
          wave's own outstanding loads have landed (polls and sleeps only);
      [2] ticks of every wave's run, from its start to its exit.
      [1] / [2] is the share of wave time spent in the ordering wait.  The
-     atomic and comparison variants add to [2] only.  Instrumented calls add
-     a few atomics per wave; the results are the same bits. */
+     atomic and comparison variants leave the counters unchanged.  A wave
+     keeps its counts in registers and adds them with three atomics when it
+     exits (an instrumented kernel, otherwise instruction for instruction the
+     production one); the results are the same bits. */
   unsigned long long* wait_stats;
 } dash_bwd_options_t;
 
@@ -189,8 +191,10 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
                   int causal, int schedule);
 
 /* Bytes of device workspace dash_attn_bwd_ex needs for this problem and
-   schedule (0 if the arguments are invalid).  The same for every schedule
-   except DASH_SCHED_PARTIALS, which needs room for all T_c dQ partials. */
+   schedule, under either mask (0 if the arguments are invalid).  The same for
+   every schedule except DASH_SCHED_PARTIALS, which needs room for all T_c dQ
+   partials: a workspace of this size for any other schedule serves every
+   schedule but PARTIALS, with a full or a causal mask. */
 size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule);
 
 /*

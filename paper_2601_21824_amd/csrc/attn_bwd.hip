@@ -227,15 +227,14 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
   // integers (no generic-to-LDS pointer conversion per copy)
   const uint32_t sm_lds = lds_base(&sm);
   auto lds_of = [&](const void* p) { return sm_lds + (uint32_t)((const char*)p - (const char*)&sm); };
-  // L * log2(e) and D of every row of every head (row bh * N + r)
-  const auto rls = make_rsrc(a.lse2, (uint32_t)((size_t)a.bh * N * 4));
-  const auto rds = make_rsrc(a.dvec, (uint32_t)((size_t)a.bh * N * 4));
   // Shift-type orders are conflict-free: the next contributor to a block reaches
-  // it at least one step later, so the counter release can wait until the next
-  // step's barrier, by which time the accumulator stores have drained.
+  // it at least one step later, so the counter release can wait until the
+  // second MFMA run of the next step, by which time the accumulator stores
+  // have drained without a wait of their own.
   const bool deferred = G.sched == S_SHIFT || G.sched == S_SYMSHIFT;
   bool failed = false;  // this wave hit a wait timeout: skip further waits
-  if constexpr (STATS) stats_wave_begin(a.wait_stats, l);
+  WaitStats wst;
+  if constexpr (STATS) stats_wave_begin(wst);
 
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(ticket, 1);
@@ -254,6 +253,11 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     const auto racc = make_rsrc(a.dqacc + (size_t)bh * a.nblk * BM * D, (uint32_t)a.nblk * BM * D * 4);
     int* ctr_head = a.counters + (size_t)bh * a.nblk * kCtrStride;
     const auto rctr = make_rsrc(ctr_head, (uint32_t)a.nblk * kCtrStride * 4);
+    // L * log2(e) and D of this head's N rows: the padded rows of a ragged
+    // last block read 0, so P = 1 there, multiplied by Q and dO rows that
+    // also read 0: those rows add exactly nothing to dK and dV
+    const auto rls = make_rsrc(a.lse2 + (size_t)bh * N, (uint32_t)N * 4);
+    const auto rds = make_rsrc(a.dvec + (size_t)bh * N, (uint32_t)N * 4);
 
     const unsigned* tab = a.steps + (size_t)wch * a.step_cap;
     const int nsteps = __builtin_amdgcn_readfirstlane((int)tab[0]);
@@ -290,7 +294,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       dma16_pair(rq, rdo, at, at + (uint32_t)sizeof(sm.qs), off, 4096u * k);
     };
     auto load_ld = [&](int pb, int b) {  // L * log2(e) and D of the block's rows
-      const uint32_t row = (uint32_t)(bh * N + pb * BM + fresh_lane());  // < 2^30 (checked by the library)
+      const uint32_t row = (uint32_t)(pb * BM + fresh_lane());
       if (w == 0) dma4(rls, lds_of(&sm.ls[b][0]), row * 4);
       if (w == 1) dma4(rds, lds_of(&sm.ds[b][0]), row * 4);
     };
@@ -452,7 +456,8 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       // {2(k%2), 2(k%2)+1}; L and D of the next row group are read one piece
       // ahead.  Element (qb, r) is query 32qb + 8(r/4) + 4g + r%4 of the block
       // and key 32w + lc of the tile.  Keys past N need no mask: their K, V
-      // rows read as zero and their dK, dV rows are not stored.
+      // rows read as zero, P is at most 1 there (exp2_unit) and their dK, dV
+      // rows are not stored.
       const int kvl = 32 * w + lc;
       const int thr = j * BC + kvl - q0 - 4 * g;  // causal: masked iff 32qb+8rb+c < thr
       bf16x8 pbf[2][2], dsbf[2][2];
@@ -473,7 +478,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
           const int c = 2 * (k & 1) + cc, r = 4 * rb + c;
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, -Lc[c]));
+          float p = exp2_unit(__builtin_fmaf(s[qb][r], c2, -Lc[c]));
           if (CAUSAL) p = (32 * qb + 8 * rb + c < thr) ? 0.f : p;
           s[qb][r] = p;
           dp[qb][r] = p * (dp[qb][r] - Dc[c]);
@@ -552,6 +557,18 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           if (early_acc && (p & 3) == 0 && p < NACC) acc_copy(pb, p >> 2);
         }
       });
+      if (early_acc) vm_rel += NACC;
+      // deferred release of the previous block, after the second run: its
+      // accumulator stores were followed by vm_rel operations (this step's
+      // prefetch and accumulator fetch), and vector memory operations
+      // complete in issue order, so at most vm_rel in flight means the stores
+      // are done.  Released this early, the block's next contributor (a step
+      // or more behind under Shift and Symmetric Shift) finds its turn at its
+      // early look instead of waiting at the end of its step.
+      if (pend_ctr >= 0) {
+        vm_wait_le(vm_rel);
+        release();
+      }
       // run 3: dV/dK of half 0, with softmax of half 1
       dvdk(0, [&](int k) {
 #pragma unroll
@@ -565,15 +582,6 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
         }
       });
 
-      if (early_acc) vm_rel += NACC;
-      // deferred release of the previous block: its accumulator stores were
-      // followed by vm_rel operations (this step's prefetch and accumulator
-      // fetch), and vector memory operations complete in issue order, so at
-      // most vm_rel in flight means the stores are done
-      if (pend_ctr >= 0) {
-        vm_wait_le(vm_rel);
-        release();
-      }
       if constexpr (MODE == kModeNoDq) {
         // dK, dV only: the next block's Q / dO have landed before the barrier
         vm_wait<0>();
@@ -627,7 +635,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
             if constexpr (STATS) vm_wait<0>();  // time the wait only, not this wave's own loads
             const unsigned long long t0 = STATS ? clock_now() : 0ull;
             have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
-            if constexpr (STATS) stats_wait(a.wait_stats, l, t0);
+            if constexpr (STATS) stats_wait(wst, t0);
             if (!have_turn) {
               failed = true;
               __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -736,7 +744,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
     if (cur_j >= 0) store_dkdv(cur_j);
     __syncthreads();  // sm.item is rewritten by the next ticket
   }
-  if constexpr (STATS) stats_wave_end(a.wait_stats, l);
+  if constexpr (STATS) stats_wave_end(wst, a.wait_stats, l);
 }
 
 template <int D, bool CAUSAL>

@@ -81,7 +81,8 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   // step's dV/dK work has covered the store latency.
   const bool deferred = G.sched == S_SHIFT || G.sched == S_SYMSHIFT;
   bool failed = false;
-  if constexpr (STATS) stats_wave_begin(a.wait_stats, l);
+  WaitStats wst;
+  if constexpr (STATS) stats_wave_begin(wst);
 
   for (;;) {
     if (tid == 0) sm.item = atomicAdd(ticket, 1);
@@ -263,8 +264,8 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
 
       // ---- P = exp(S - L), dS = P (dP - D).  Element (qb, r) is query
       //      16qb + 4(l/16) + r of the block and key 16w + l%16 of the tile.
-      //      Keys past N need no mask: their K, V rows read as zero and their
-      //      dK, dV rows are not stored.
+      //      Keys past N need no mask: their K, V rows read as zero, P is at
+      //      most 1 there (exp2_unit) and their dK, dV rows are not stored.
       const int kvl = 16 * w + lr;
       const int thr = j * BC + kvl - q0 - 4 * gq;  // causal: masked iff 16qb + r < thr
 #pragma unroll
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
         const f32x4 D4 = *(const f32x4*)&sm.ds[16 * qb + 4 * gq];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][r], c2, -L4[r]));
+          float p = exp2_unit(__builtin_fmaf(s[qb][r], c2, -L4[r]));
           if (CAUSAL) p = (16 * qb + r < thr) ? 0.f : p;
           s[qb][r] = p;
           dp[qb][r] = p * (dp[qb][r] - D4[r]);
@@ -364,7 +365,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
           if constexpr (STATS) vm_wait<0>();  // time the wait only, not this wave's own loads
           const unsigned long long t0 = STATS ? clock_now() : 0ull;
           have_turn = wait_turn(ctr, NW * rank, a.spin_limit);
-          if constexpr (STATS) stats_wait(a.wait_stats, l, t0);
+          if constexpr (STATS) stats_wait(wst, t0);
           if (!have_turn) {
             failed = true;
             __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -426,7 +427,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
     if (cur_j >= 0) store_dkdv(cur_j);
     __syncthreads();  // sm.item is rewritten by the next ticket
   }
-  if constexpr (STATS) stats_wave_end(a.wait_stats, l);
+  if constexpr (STATS) stats_wave_end(wst, a.wait_stats, l);
 }
 
 }  // namespace

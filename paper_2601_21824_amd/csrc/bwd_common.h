@@ -27,21 +27,26 @@ __device__ inline bool wait_turn(const int* ctr, int want, int limit) {
   return true;
 }
 
-// Ordering-wait statistics (instrumented kernels only): lane 0 of each wave
-// subtracts its start time from st[2] and adds its exit time, and adds one to
-// st[0] and the ticks it spent to st[1] for every wait at the end of a step
-// (the turn was not visible at the early look).  Real-time clock ticks.
+// Ordering-wait statistics (instrumented kernels only).  Each wave counts
+// its late wave-steps (the turn was not visible at the early look) and the
+// real-time clock ticks their waits took in its own registers, and publishes
+// them, with its lifetime, by three atomic adds of lane 0 when it exits: an
+// atomic on the shared counters at every late step would serialize the waves
+// on those addresses and distort the waits being measured.
+struct WaitStats {
+  unsigned long long begin = 0, late = 0, ticks = 0;
+};
 __device__ inline unsigned long long clock_now() { return (unsigned long long)__builtin_amdgcn_s_memrealtime(); }
-__device__ inline void stats_wave_begin(unsigned long long* st, int lane) {
-  if (lane == 0) atomicAdd(&st[2], 0ull - clock_now());
+__device__ inline void stats_wave_begin(WaitStats& w) { w.begin = clock_now(); }
+__device__ inline void stats_wait(WaitStats& w, unsigned long long t0) {
+  w.late += 1;
+  w.ticks += clock_now() - t0;
 }
-__device__ inline void stats_wave_end(unsigned long long* st, int lane) {
-  if (lane == 0) atomicAdd(&st[2], clock_now());
-}
-__device__ inline void stats_wait(unsigned long long* st, int lane, unsigned long long t0) {
+__device__ inline void stats_wave_end(const WaitStats& w, unsigned long long* st, int lane) {
   if (lane == 0) {
-    atomicAdd(&st[0], 1ull);
-    atomicAdd(&st[1], clock_now() - t0);
+    atomicAdd(&st[0], w.late);
+    atomicAdd(&st[1], w.ticks);
+    atomicAdd(&st[2], clock_now() - w.begin);
   }
 }
 

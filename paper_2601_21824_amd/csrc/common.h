@@ -54,6 +54,17 @@ __device__ inline void st4f(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, 0);
 }
 
+// P = 2^x clamped to [0, 1]; the clamp is the exp instruction's own output
+// modifier, so it costs nothing.  For a real key x = S*log2(e) - L*log2(e) <= 0
+// up to rounding (a score never exceeds its row's logsumexp), so the clamp
+// only removes rounding excess.  A padded key of a ragged last KV tile has
+// S = 0 (its K row reads as zero): 2^(-L*log2(e)) would overflow to inf for a
+// row whose logsumexp is below about -88, and inf * 0 would put NaN into dQ;
+// clamped it is 1, and every product it enters has a zero K or V factor.
+__device__ inline float exp2_unit(float x) {
+  return __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(x), 0.f, 1.f);
+}
+
 // fp32 -> bf16 with round-to-nearest-even (hardware v_cvt_pk_bf16_f32)
 __device__ inline unsigned pack_bf16(float lo, float hi) {
   typedef __bf16 bf16x2 __attribute__((__vector_size__(4)));

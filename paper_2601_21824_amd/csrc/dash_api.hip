@@ -33,8 +33,10 @@ struct Layout {
 };
 
 // ctrl first so that dash_bwd_check can find it without the problem size.
-// `sched` is a resolved schedule: PARTIALS keeps one accumulator-sized buffer
-// per KV tile.
+// The layout depends on the schedule only through PARTIALS, which keeps one
+// accumulator-sized buffer per KV tile: the step and ticket tables are sized
+// for the longest chains and the most chains of any schedule and mask, so a
+// workspace sized for one schedule serves every other one (and both masks).
 Layout layout(int B, int H, int N, int d, int sched) {
   Layout L;
   const size_t bh = (size_t)B * H;
@@ -52,10 +54,12 @@ Layout layout(int B, int H, int N, int d, int sched) {
   off += align256(bh * N * sizeof(float));
   L.counters = off;
   off += align256(bh * nblk * dash::kCtrStride * sizeof(int));
-  // per-chain step tables: at most T_c + 1 chains (Symmetric Shift pads T_c),
-  // each its length and at most (T_r + 1) * nsub steps; then the ticket order
-  const dash::Geom G = dash::make_geom(sched, 0, N, d);
-  const dash::Geom Gc = dash::make_geom(sched, 1, N, d);
+  // per-chain step tables: at most T_c + 1 chains (Symmetric Shift pads T_c
+  // to even), each its length and at most (T_r + 1) * nsub steps (full mask:
+  // 64-row Q tiles; causal: Symmetric Shift's padded T_r + 1 tasks); then the
+  // ticket order
+  const dash::Geom G = dash::make_geom(dash::S_SHIFT, 0, N, d);
+  const dash::Geom Gc = dash::make_geom(dash::S_SYMSHIFT, 1, N, d);
   const int cap_f = (G.t_r + 1) * G.nsub, cap_c = (Gc.t_r + 1) * Gc.nsub;
   L.step_cap = 1 + (cap_f > cap_c ? cap_f : cap_c);
   const size_t chains = (size_t)(G.t_c > Gc.t_c ? G.t_c : Gc.t_c) + 1;
@@ -134,7 +138,7 @@ int check_shape(int B, int H, int N, int d) {
   if (d != 64 && d != 128 && d != 256) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64, 128 or 256");
   if ((double)N * d * 4 >= 2147483648.0) return fail(DASH_ERR_INVALID_ARG, "N*d too large (per-head fp32 > 2 GiB)");
   if ((double)B * H >= 2147483647.0 / 1024) return fail(DASH_ERR_INVALID_ARG, "B*H too large");
-  // L and D of all rows are addressed with 32-bit byte offsets (4 bytes per row)
+  // the interface's documented row limit (row counts stay far inside int range)
   if ((double)B * H * N >= 1073741824.0) return fail(DASH_ERR_INVALID_ARG, "B*H*N too large (at most 2^30 - 1 rows)");
   return DASH_OK;
 }
@@ -239,7 +243,7 @@ int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float
 
 int dash_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N, int d,
                   int causal) {
-  if (d <= 0) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64 or 128");
+  if (d != 64 && d != 128 && d != 256) return fail(DASH_ERR_INVALID_ARG, "head dim d must be 64, 128 or 256");
   return dash_attn_fwd_ex(q, k, v, o, lse, B, H, N, d, causal, 1.0f / std::sqrt((float)d), nullptr);
 }
 

@@ -159,3 +159,32 @@ def test_missing_library_raises_instead_of_falling_back():
         "print('ok')\n")
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0 and "ok" in r.stdout, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("N,d", [(8000, 128), (8192, 128), (1000, 64), (32704, 256), (32768, 256), (333, 256)])
+@pytest.mark.parametrize("sized_for", ["shift", "auto", "naive", "descending", "atomic", "split"])
+def test_workspace_size_serves_every_schedule_and_mask(N, d, sized_for):
+    """A workspace of dash_bwd_workspace_size(..., s) bytes passes the size
+    check of dash_attn_bwd_ex for every schedule but PARTIALS under both masks
+    -- including causal SHIFT, which runs as Symmetric Shift with T_c padded to
+    even (odd T_c at N = 8000, d = 128 and N = 32704, d = 256).  The call is
+    stopped right after the size check by an invalid option, so no device is
+    touched; one byte less is reported as a workspace error."""
+    lib = b.load()
+    B, H = 2, 3
+    ws = b.dash_bwd_workspace_size(B, H, N, d, sized_for)
+    assert ws > 0
+    p = [ctypes.c_void_p(1 << 20)] * 9
+    bad_opts = b.dash_bwd_options_t(-1)  # spin_limit < 0: checked right after the workspace
+    for causal in (0, 1):
+        for sched in ("atomic", "naive", "descending", "shift", "symshift", "auto", "split"):
+            if sched == "symshift" and not causal:
+                continue
+            if sched == "split" and d > 128:
+                continue
+            args = (*p, B, H, N, d, causal, b.SCHEDULES[sched], ctypes.c_float(0.125), ctypes.c_void_p(1 << 20))
+            rc = lib.dash_attn_bwd_ex(*args, ws, ctypes.byref(bad_opts), None)
+            assert rc == b.DASH_ERR_INVALID_ARG and "spin_limit" in b.dash_last_error(), (sched, causal)
+            need = b.dash_bwd_workspace_size(B, H, N, d, sched)
+            rc = lib.dash_attn_bwd_ex(*args[:-1], ctypes.c_void_p(1 << 20), need - 1, ctypes.byref(bad_opts), None)
+            assert rc == b.DASH_ERR_INVALID_ARG and "workspace" in b.dash_last_error(), (sched, causal)

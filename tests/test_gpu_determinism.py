@@ -29,8 +29,14 @@ DET_CASES = [  # (B, H, N, d, causal, schedule[, placement])
     # XCD-local placement: several workgroups of one head on each XCD read
     # the accumulator slots that the others wrote just before
     (4, 16, 1024, 64, True, "descending", 2),
+    (4, 16, 1024, 64, True, "naive", 2),
     (2, 8, 2048, 128, False, "shift", 2),
     (2, 8, 1024, 256, True, "naive", 2),
+    # the full-size workloads: the benchmark's Shift (16384 tokens, 16 heads
+    # of 128, full mask) and the causal schedules at N = 8192 (32 heads of 128)
+    (2, 16, 8192, 128, False, "shift"),
+    (2, 32, 8192, 128, True, "descending"),
+    (2, 32, 8192, 128, True, "symshift"),
 ]
 
 
@@ -367,16 +373,26 @@ def test_watchdog_reports_timeout_and_library_recovers():
 
 
 def test_atomic_variant_run_to_run_deviation_reported():
-    """The atomic variant is only reported (cf. Table 1): print the mean over
-    runs of max |dQ_r - dQ_1|; it must still be within tolerance every run."""
+    """The atomic variant's run-to-run deviation is only reported (cf. Table 1):
+    print the mean over runs of max |dQ_r - dQ_1|.  Every run must still match
+    the oracle within the tolerance (sampled dQ, dK, dV rows of the first and
+    last head), whatever order its atomic adds landed in."""
+    from gpu_util import assert_close
     B, H, N, d, causal = 2, 16, 2048, 128, True
-    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=13)
+    q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=13)
     og, lseg = run_fwd(qg, kg, vg, causal)
+    rows = np.array([0, 1, 63, 64, 1000, 2046, 2047])
+    heads = ((0, 0), (B - 1, H - 1))
+    refs = {bh: oracle.attn_bwd(q[bh], k[bh], v[bh], do[bh], causal, dq_rows=rows, kv_rows=rows) for bh in heads}
     ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, "atomic")
     devs = []
-    for _ in range(9):
-        dq, _, _ = run_bwd(qg, kg, vg, og, dog, lseg, causal, "atomic")
-        devs.append(float((dq.float() - ref[0].float()).abs().max()))
+    for r in range(10):
+        out = ref if r == 0 else run_bwd(qg, kg, vg, og, dog, lseg, causal, "atomic")
+        for bh in heads:
+            for name, got, want in zip(("dQ", "dK", "dV"), out, refs[bh][:3]):
+                assert_close(f"run {r + 1} {name} head {bh}", got[bh][rows], want[rows])
+        if r:
+            devs.append(float((out[0].float() - ref[0].float()).abs().max()))
     print(f"\n[atomic] mean max|dQ_r - dQ_1| over 9 runs: {np.mean(devs):.3e}", flush=True)
 
 

@@ -1,7 +1,8 @@
 """GPU parity: every schedule of the HIP backward (and the forward that feeds
 it) against the fp64 oracle, element by element, at sizes that span several
-tiles, ragged tails and both masks; plus sampled outputs at the full
-benchmark size (B=2, H=16, N=8192, d=128, full mask) and at the long-sequence
+tiles, ragged tails and both masks; plus sampled outputs at the full sizes of
+the workloads: the 16384-token sweeps at N = 8192 (16 heads of 128, full
+mask; 32 heads of 128, causal) and N = 16384, and the long-sequence
 head-dim-256 workload (B=1, H=8, N=32768, d=256, both masks)."""
 import numpy as np
 import pytest
@@ -9,6 +10,7 @@ import torch
 
 import oracle
 from gpu_util import assert_close, inputs, run_bwd, run_fwd, schedules
+from paper_2601_21824_amd.synth import make_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -65,40 +67,91 @@ def test_backward_all_schedules_match_oracle(case):
             print(f"    {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
 
 
-@pytest.mark.parametrize("sched", ["shift", "naive", "atomic"])
-def test_full_size_sampled(sched):
-    """The benchmark workload at full size; sampled dQ rows and dK/dV rows of
-    the first and last head against the oracle, which computes those rows one
-    by one (L and D of every query row of the sampled heads)."""
-    B, H, N, d, causal = 2, 16, 8192, 128, False
-    print(f"\n[sampled] B={B} H={H} N={N} d={d} schedule={sched}", flush=True)
-    key = ("full", B, H, N, d)
+def sample_rows(N, edges, count, seed):
+    """Hand-picked edge rows plus `count` rows drawn uniformly (seeded).  The
+    relative Frobenius error is taken over the uniform rows only -- an
+    unbiased estimate of the whole tensor's; edge rows (a causal row 1 sees
+    two keys and has a gradient many times the typical row's) would weight it
+    arbitrarily -- and the per-element bound over all of them."""
+    rng = np.random.default_rng(seed)
+    uni = np.sort(rng.choice(N, size=min(count, N), replace=False))
+    return np.array(sorted(set(edges) | set(uni.tolist()))), uni
+
+
+def assert_close_sampled(name, got, ref, rows, uni):
+    """got / ref: [N, d] with valid entries at `rows`."""
+    from gpu_util import errors
+    rf, _ = errors(got[uni], ref[uni])
+    _, rm = errors(got[rows], ref[rows])
+    assert rf <= 5e-3 and rm <= 2e-2, f"{name}: rel_frob={rf:.3e} (uniform rows) rel_max={rm:.3e}"
+    return rf, rm
+
+
+# (B, H, N, d, causal, schedule): the 16384-token sweeps' N = 8192 points --
+# the benchmark workload (16 heads of 128, full mask) and the causal sweep
+# (32 heads of 128) -- whole first and last heads against the oracle
+FULL_HEADS = [
+    (2, 16, 8192, 128, False, "shift"),
+    (2, 16, 8192, 128, False, "naive"),
+    (2, 16, 8192, 128, False, "atomic"),
+    (2, 32, 8192, 128, True, "descending"),
+    (2, 32, 8192, 128, True, "symshift"),
+    (2, 32, 8192, 128, True, "atomic"),
+]
+
+
+@pytest.mark.parametrize("case", FULL_HEADS, ids=[f"B{c[0]}H{c[1]}N{c[2]}{'c' if c[4] else 'f'}-{c[5]}" for c in FULL_HEADS])
+def test_full_size_whole_heads(case):
+    """Full-size workloads: every dQ, dK, dV (and O) entry of the first and
+    last head against the oracle; over every head, sum_j dV_j = sum_i dO_i
+    (rows of P sum to one)."""
+    B, H, N, d, causal, sched = case
+    print(f"\n[heads] B={B} H={H} N={N} d={d} causal={causal} schedule={sched}", flush=True)
+    key = ("heads", B, H, N, d, causal)
+    heads = ((0, 0), (B - 1, H - 1))
     if key not in _cache:
         q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=5)
         og, lseg = run_fwd(qg, kg, vg, causal)
-        rows = np.array([0, 1, 63, 64, 127, 4095, 4096, 8000, 8190, 8191])
-        refs = {}
-        for (b, h) in ((0, 0), (1, 15)):
-            refs[(b, h)] = oracle.attn_bwd(q[b, h], k[b, h], v[b, h], do[b, h], causal,
-                                           dq_rows=rows, kv_rows=rows)
-            ro, rl = oracle.attn_fwd(q[b, h], k[b, h], v[b, h], causal, rows=rows)
-            refs[(b, h, "fwd")] = (ro, rl)
+        refs = {bh: oracle.attn_bwd(q[bh], k[bh], v[bh], do[bh], causal) for bh in heads}
+        fwd = {bh: oracle.attn_fwd(q[bh], k[bh], v[bh], causal) for bh in heads}
         _cache.clear()
-        _cache[key] = (qg, kg, vg, dog, og, lseg, rows, refs)
-    qg, kg, vg, dog, og, lseg, rows, refs = _cache[key]
+        _cache[key] = (qg, kg, vg, dog, og, lseg, refs, fwd)
+    qg, kg, vg, dog, og, lseg, refs, fwd = _cache[key]
     dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
-    for (b, h) in ((0, 0), (1, 15)):
-        rdq, rdk, rdv, _, _ = refs[(b, h)]
-        ro, rl = refs[(b, h, "fwd")]
-        assert_close("O rows", og[b, h][rows], ro[rows])
-        for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
-            rf, rm = assert_close(f"{sched} {name} head({b},{h})", got[b, h][rows], ref[rows])
-            print(f"    head({b},{h}) {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
-    # property over every head: rows of P sum to one, so sum_j dV_j = sum_i dO_i
+    for bh in heads:
+        assert_close("O", og[bh], fwd[bh][0])
+        for name, got, ref in zip(("dQ", "dK", "dV"), (dq, dk, dv), refs[bh][:3]):
+            rf, rm = assert_close(f"{sched} {name} head{bh}", got[bh], ref)
+            print(f"    head{bh} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
     sv = dv.float().sum(dim=2)
     so = dog.float().sum(dim=2)
     rel = (sv - so).norm() / so.norm()
     assert rel < 5e-3, float(rel)
+
+
+@pytest.mark.parametrize("sched", ["shift", "naive", "atomic"])
+def test_n16384_sampled(sched):
+    """The 16384-token full-mask sweep at N = 16384 (B=1, 16 heads of 128):
+    sampled dQ and dK/dV rows of the first and last head (edges plus uniform
+    rows) against the oracle, which computes those rows one by one."""
+    B, H, N, d, causal = 1, 16, 16384, 128, False
+    print(f"\n[sampled] B={B} H={H} N={N} d={d} schedule={sched}", flush=True)
+    key = ("n16384",)
+    heads = ((0, 0), (B - 1, H - 1))
+    if key not in _cache:
+        q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=6)
+        og, lseg = run_fwd(qg, kg, vg, causal)
+        rows, uni = sample_rows(N, (0, 1, 63, 64, 127, 128, 8191, 8192, N - 2, N - 1), 48, seed=16384)
+        refs = {bh: oracle.attn_bwd(q[bh], k[bh], v[bh], do[bh], causal, dq_rows=rows, kv_rows=rows) for bh in heads}
+        _cache.clear()
+        _cache[key] = (qg, kg, vg, dog, og, lseg, rows, uni, refs)
+    qg, kg, vg, dog, og, lseg, rows, uni, refs = _cache[key]
+    dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
+    for bh in heads:
+        for name, got, ref in zip(("dQ", "dK", "dV"), (dq, dk, dv), refs[bh][:3]):
+            g = got[bh].float().cpu().double().numpy()
+            rf, rm = assert_close_sampled(f"{sched} {name} head{bh}", g, ref, rows, uni)
+            print(f"    head{bh} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
 
 
 LONG = [(False, "shift"), (False, "naive"), (False, "atomic"), (True, "symshift"), (True, "descending")]
@@ -107,32 +160,38 @@ LONG = [(False, "shift"), (False, "naive"), (False, "atomic"), (True, "symshift"
 @pytest.mark.parametrize("causal,sched", LONG, ids=[f"{'c' if c else 'f'}-{s}" for c, s in LONG])
 def test_long_d256_sampled(causal, sched):
     """B=1, H=8, N=32768, d=256, inputs ~N(0, 0.5^2), both masks.  Full-mask
-    Shift runs as two groups of 256 KV-tile chains.  Sampled dQ and O rows of
-    the first and last head against the oracle (rows computed one by one);
-    dK and dV through properties that hold at any size: every row of dS sums
-    to zero, so sum_j dK_j = 0, and every row of P sums to one, so
-    sum_j dV_j = sum_i dO_i."""
+    Shift runs as two groups of 256 KV-tile chains (64-row tiles).  Sampled
+    rows -- the first and last rows, both sides of a KV-tile boundary and of
+    the Shift group boundary at KV row 256 * 64 = 16384, the last block, and
+    40 rows drawn uniformly -- against the oracle, which computes them one by
+    one: dQ and O of the first and last head, dK and dV of the first head,
+    element by element; and over every head the properties that hold at any
+    size: every row of dS sums to zero, so sum_j dK_j = 0, and every row of P
+    sums to one, so sum_j dV_j = sum_i dO_i."""
     B, H, N, d = 1, 8, 32768, 256
     print(f"\n[long] B={B} H={H} N={N} d={d} causal={causal} schedule={sched}", flush=True)
     key = ("long", causal)
     if key not in _cache:
         q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=11, sigma=0.5)
         og, lseg = run_fwd(qg, kg, vg, causal)
-        rows = np.array([0, 1, 63, 64, 4095, 16384, 32704, 32767])
+        rows, uni = sample_rows(N, (0, 1, 63, 64, 4095, 16383, 16384, 32704, 32767), 40, seed=32768)
         refs = {}
         for h in (0, H - 1):
-            refs[h] = oracle.attn_bwd(q[0, h], k[0, h], v[0, h], do[0, h], causal, dq_rows=rows, kv_rows=[])
+            refs[h] = oracle.attn_bwd(q[0, h], k[0, h], v[0, h], do[0, h], causal, dq_rows=rows,
+                                      kv_rows=rows if h == 0 else [])
             refs[(h, "fwd")] = oracle.attn_fwd(q[0, h], k[0, h], v[0, h], causal, rows=rows)
         _cache.clear()
-        _cache[key] = (qg, kg, vg, dog, og, lseg, rows, refs)
-    qg, kg, vg, dog, og, lseg, rows, refs = _cache[key]
+        _cache[key] = (qg, kg, vg, dog, og, lseg, rows, uni, refs)
+    qg, kg, vg, dog, og, lseg, rows, uni, refs = _cache[key]
     dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
     for h in (0, H - 1):
-        rdq = refs[h][0]
+        rdq, rdk, rdv, _, _ = refs[h]
         ro, _ = refs[(h, "fwd")]
-        assert_close("O rows", og[0, h][rows], ro[rows])
-        rf, rm = assert_close(f"{sched} dQ head {h}", dq[0, h][rows], rdq[rows])
-        print(f"    head {h} dQ: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
+        assert_close_sampled("O rows", og[0, h].float().cpu().double().numpy(), ro, rows, uni)
+        checks = (("dQ", dq, rdq),) + ((("dK", dk, rdk), ("dV", dv, rdv)) if h == 0 else ())
+        for name, got, ref in checks:
+            rf, rm = assert_close_sampled(f"{sched} {name} head {h}", got[0, h].float().cpu().double().numpy(), ref, rows, uni)
+            print(f"    head {h} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
     dkf, dvf = dk.float(), dv.float()
     zero = dkf.sum(dim=2).norm() / dkf.norm()
     sv = dvf.sum(dim=2)
@@ -140,3 +199,43 @@ def test_long_d256_sampled(causal, sched):
     rel = (sv - so).norm() / so.norm()
     print(f"    |sum_j dK_j| / |dK| = {float(zero):.2e}, sum_j dV_j vs sum_i dO_i: {float(rel):.2e}", flush=True)
     assert zero < 1e-2 and rel < 5e-3, (float(zero), float(rel))
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("causal", [False, True])
+def test_ragged_tail_next_head_with_very_negative_lse(d, causal):
+    """N = 200 leaves padded query rows in each head's last 64-row block and
+    padded keys in its last KV tile.  Query 0 of head 1 is built with a
+    logsumexp far below -88 (natural log): with a causal mask it sees only key
+    0, and q_0 . k_0 is very negative; with a full mask the first coordinate of
+    every key of head 1 is made |k_j1| + 2 > 0 and q_0 points the other way
+    along it.  Its dO row is zero, so dS of that row is exactly zero and the
+    row adds nothing to any gradient (only its L is extreme).  Two ways this
+    could overflow P = exp(S - L) to inf, where inf * 0 turns real gradients
+    into NaN: the padded rows of head 0 must read L = D = 0 within their own
+    head's bounds, not head 1's first row; and the padded keys of head 1
+    (S = 0, their K rows read as zero) must not give P = exp(-L) in row 0.
+    Every schedule against the oracle."""
+    B, H, N = 1, 2, 200
+    q, k, v, do = make_inputs(B, H, N, d, seed=404)
+    q, k, do = q.clone(), k.clone(), do.clone()
+    q[0, 1, 0] = 0.0
+    do[0, 1, 0] = 0.0
+    if causal:
+        q[0, 1, 0, 0] = 2048.0
+        k[0, 1, 0] = 0.0
+        k[0, 1, 0, 0] = -1.0
+    else:
+        q[0, 1, 0, 0] = -1024.0
+        k[0, 1, :, 0] = k[0, 1, :, 0].abs() + 2.0
+    qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
+    ref_o, ref_l = oracle.attn_fwd(q, k, v, causal)
+    assert ref_l[0, 1, 0] < -100.0
+    rdq, rdk, rdv, _, _ = oracle.attn_bwd(q, k, v, do, causal)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    assert_close("O", og, ref_o)
+    for sched in schedules(causal, d):
+        dq, dk, dv = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
+        for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
+            rf, rm = assert_close(f"{sched} {name}", got, ref)
+            print(f"  {sched} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
