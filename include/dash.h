@@ -16,8 +16,9 @@
  *    query i sees key j iff j <= i.
  *  - d must be 64, 128 or 256.  N >= 0 is arbitrary (ragged last tiles are masked);
  *    B, H >= 0, B*H*N < 2^30.  A problem with B*H*N == 0 is a successful no-op.
- *  - scale is the softmax scale s in S = s * Q K^T (the _ex forms take it;
- *    the others use 1/sqrt(d)).  dQ and dK include the factor s, dV does not.
+ *  - scale is the softmax scale s in S = s * Q K^T (the _ex and _noalloc
+ *    forms take it, 0 selecting 1/sqrt(d); the others use 1/sqrt(d)).  dQ and
+ *    dK include the factor s, dV does not.
  *  - Calls are asynchronous on the given HIP stream (hipStream_t passed as
  *    void*; NULL = the default stream) unless stated otherwise.
  *  - No C++ exception crosses this interface.  Every int-returning function
@@ -207,6 +208,27 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
                      const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,
                      int causal, int schedule, float scale, void* workspace, size_t ws_bytes,
                      const dash_bwd_options_t* opts, void* stream);
+
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the backward of
+ * dash_attn_bwd_ex with default options, on a fixed workspace that the
+ * library holds on every device it runs on -- a 256 MiB array in device
+ * memory, present from the library's load until the process ends.  The call
+ * allocates nothing (its first call on a device looks the array's address up
+ * once).  Problems whose dash_bwd_workspace_size exceeds 256 MiB (e.g. more
+ * than B*H*N*d = 64 Mi elements) are rejected with DASH_ERR_UNSUPPORTED.
+ * Asynchronous on `stream`; every call on a device uses that device's one
+ * array, so calls that overlap in time on one device (other streams, other
+ * threads) race and must be serialized by the caller.  The kernels reset what
+ * must start at zero themselves (no memset is recorded).  status: optional
+ * caller-owned device int; the call sets it to 0, or to 1 if an ordering wait
+ * timed out (outputs then undefined) -- read it once the stream has finished
+ * the call.  Argument errors as dash_attn_bwd_ex.
+ */
+int dash_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dO,
+                          const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal,
+                          int schedule, float scale, int* status, void* stream);
 
 /* Synchronizes `stream`, then returns DASH_ERR_TIMEOUT if the last backward
    that used `workspace` hit a wait timeout, DASH_OK otherwise. */

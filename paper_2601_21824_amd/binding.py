@@ -8,7 +8,6 @@ module raises -- there is no fallback path.
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 
 import numpy as np
@@ -28,7 +27,7 @@ DASH_PLACEMENT_AUTO, DASH_PLACEMENT_GLOBAL, DASH_PLACEMENT_XCD = 0, 1, 2
 
 # every symbol include/dash.h declares
 EXPORTS = ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_bwd_workspace_size",
-           "dash_attn_bwd_ex", "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table",
+           "dash_attn_bwd_ex", "dash_attn_bwd_noalloc", "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table",
            "dash_bwd_placement", "dash_mfma_peak", "dash_last_error", "dash_release_workspace")
 
 
@@ -64,6 +63,7 @@ def load():
         lib.dash_attn_bwd.argtypes = [vp] * 9 + [ci] * 6
         lib.dash_attn_bwd_ex.argtypes = ([vp] * 9 + [ci] * 6 + [cf, vp, sz,
                                          ctypes.POINTER(dash_bwd_options_t), vp])
+        lib.dash_attn_bwd_noalloc.argtypes = [vp] * 9 + [ci] * 6 + [cf, vp, vp]
         lib.dash_bwd_workspace_size.argtypes = [ci] * 5
         lib.dash_bwd_workspace_size.restype = sz
         lib.dash_bwd_check.argtypes = [vp, vp]
@@ -73,7 +73,7 @@ def load():
         lib.dash_mfma_peak.argtypes = [ci, ctypes.POINTER(ctypes.c_double)]
         lib.dash_last_error.restype = ctypes.c_char_p
         lib.dash_release_workspace.restype = None
-        for f in ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_attn_bwd_ex",
+        for f in ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_attn_bwd_ex", "dash_attn_bwd_noalloc",
                   "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table", "dash_bwd_placement",
                   "dash_mfma_peak"):
             getattr(lib, f).restype = ci
@@ -137,7 +137,7 @@ def dash_attn_fwd(q, k, v, o, lse, causal: bool, scale=None, stream=None):
     B, H, N, d = _shape(q)
     _require((q, k, v, o), "bf16")
     _require((lse,), "f32")
-    s = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    s = 0.0 if scale is None else float(scale)  # 0: the library's default 1/sqrt(d)
     _check(load().dash_attn_fwd_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, N, d,
                                    int(causal), s, _stream(stream)))
 
@@ -159,12 +159,29 @@ def dash_attn_bwd(q, k, v, o, dO, lse, dq, dk, dv, causal: bool, schedule, scale
         return
     if workspace is None:
         raise DashError(DASH_ERR_INVALID_ARG, "scale/options need an explicit workspace")
-    s = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    s = 0.0 if scale is None else float(scale)  # 0: the library's default 1/sqrt(d)
     opt = ctypes.byref(options) if options is not None else None
     _check(lib.dash_attn_bwd_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dO), _ptr(lse),
                                 _ptr(dq), _ptr(dk), _ptr(dv), B, H, N, d, int(causal),
                                 _sched(schedule), s, _ptr(workspace), workspace.numel(), opt,
                                 _stream(stream)))
+
+
+def dash_attn_bwd_noalloc(q, k, v, o, dO, lse, dq, dk, dv, causal: bool, schedule, scale=None, status=None,
+                          stream=None):
+    """Backward into dq, dk, dv on the library's fixed per-device scratch: no
+    allocation, asynchronous on the current stream.  ``status``: optional
+    device int32 tensor (one element) that receives 0, or 1 after a wait
+    timeout, once the stream has run the call."""
+    B, H, N, d = _shape(q)
+    _require((q, k, v, o, dO, dq, dk, dv), "bf16")
+    _require((lse,), "f32")
+    if status is not None and (not status.is_cuda or status.dtype.itemsize != 4):
+        raise DashError(DASH_ERR_INVALID_ARG, "status must be a device int32 tensor")
+    s = 0.0 if scale is None else float(scale)
+    _check(load().dash_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dO), _ptr(lse),
+                                        _ptr(dq), _ptr(dk), _ptr(dv), B, H, N, d, int(causal),
+                                        _sched(schedule), s, _ptr(status), _stream(stream)))
 
 
 def dash_bwd_check(workspace, stream=None) -> int:

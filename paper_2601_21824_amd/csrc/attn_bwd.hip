@@ -68,6 +68,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(BwdArgs a, int zero_acc) {
   if (gtid == 0) {
     a.ctrl[kCtrlTicket] = 0;
     a.ctrl[kCtrlError] = 0;
+    if (a.status) *a.status = 0;
   }
   if (gtid < kMaxXcd) a.ctrl[kCtrlXcdTicket + gtid] = 0;
   // every chain's step table (the same for every head): entry 0 is the number
@@ -639,6 +640,7 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
             if (!have_turn) {
               failed = true;
               __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              if (a.status) __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             } else if (rank > 0) {
               load_acc(pb);  // late fetch: the turn came after the early poll
             }

@@ -369,6 +369,7 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
           if (!have_turn) {
             failed = true;
             __hip_atomic_store(&a.ctrl[kCtrlError], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a.status) __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           } else if (rank > 0) {
             load_acc(pb);  // late fetch: the turn came after the early poll
           }

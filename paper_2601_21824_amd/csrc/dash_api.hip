@@ -75,6 +75,7 @@ struct DeviceInfo {
   int device = -1;
   int cus = 0;
   int occ64 = 0, occ128 = 0, occ256 = 0;
+  bool probed = false;  // nxcd is known (the probe allocates, so it runs only when XCD placement is asked for)
   int nxcd = 0;  // XCDs, when workgroup i runs on XCD i % nxcd (0: not usable for XCD-local placement)
 };
 
@@ -108,7 +109,21 @@ int probe_xcds() {
 std::mutex g_mu;
 DeviceInfo g_dev[64];
 
-int device_info(DeviceInfo* out) {
+// bytes of dash_attn_bwd_noalloc's fixed workspace on each device
+constexpr size_t kScratchBytes = (size_t)256 << 20;
+
+}  // namespace
+
+// dash_attn_bwd_noalloc's workspace: each device holds its own copy from
+// module load until the process ends.
+static __device__ __align__(256) unsigned char dash_scratch[kScratchBytes];
+
+namespace {
+
+// The current device's properties (queried once per device).  With xcd, also
+// whether XCD-local placement is usable: that probe runs a kernel on a small
+// buffer it allocates, so only calls that ask for XCD placement run it.
+int device_info(DeviceInfo* out, bool xcd = false) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(DASH_ERR_NO_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
@@ -126,8 +141,11 @@ int device_info(DeviceInfo* out) {
     di.occ128 = dash::bwd_main_occupancy(128);
     di.occ256 = dash::bwd_main_occupancy(256);
     if (di.occ64 <= 0 || di.occ128 <= 0 || di.occ256 <= 0) return fail(DASH_ERR_HIP, "occupancy query failed");
-    di.nxcd = probe_xcds();
     di.device = dev;
+  }
+  if (xcd && !di.probed) {
+    di.nxcd = probe_xcds();
+    di.probed = true;
   }
   *out = di;
   return DASH_OK;
@@ -229,6 +247,7 @@ size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule) {
 int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N,
                      int d, int causal, float scale, void* stream) {
   int rc = check_shape(B, H, N, d);
+  if (scale == 0.f) scale = 1.0f / std::sqrt((float)d);
   if (rc) return rc;
   if ((size_t)B * H * N == 0) return DASH_OK;
   if (!q || !k || !v || !o || !lse) return fail(DASH_ERR_INVALID_ARG, "null tensor pointer");
@@ -247,10 +266,17 @@ int dash_attn_fwd(const void* q, const void* k, const void* v, void* o, float* l
   return dash_attn_fwd_ex(q, k, v, o, lse, B, H, N, d, causal, 1.0f / std::sqrt((float)d), nullptr);
 }
 
-int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
-                     void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule,
-                     float scale, void* workspace, size_t ws_bytes, const dash_bwd_options_t* opts,
-                     void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The backward on `workspace` (dash_attn_bwd_ex's contract); `status`, if
+// non-null, is a device int that bwd_pre zeroes and a wait timeout sets.
+int bwd_launch(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
+               void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule,
+               float scale, void* workspace, size_t ws_bytes, const dash_bwd_options_t* opts, int* status,
+               void* stream) {
+  if (scale == 0.f && d > 0) scale = 1.0f / std::sqrt((float)d);
   int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
   if (rc) return rc;
   if ((size_t)B * H * N == 0) return DASH_OK;
@@ -270,7 +296,7 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
     return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
   DeviceInfo di;
-  if ((rc = device_info(&di))) return rc;
+  if ((rc = device_info(&di, placement == DASH_PLACEMENT_XCD))) return rc;
 
   dash::Geom G = dash::make_geom(sched, causal, N, d);
   bool xcd = false;
@@ -360,9 +386,61 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
   const bool timed = opts && opts->event_main_begin && opts->event_main_end;
   a.ev_begin = timed ? (hipEvent_t)opts->event_main_begin : nullptr;
   a.ev_end = timed ? (hipEvent_t)opts->event_main_end : nullptr;
+  a.status = status;
   hipError_t e = dash::launch_bwd(a, d, grid, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "backward launch");
   return DASH_OK;
+}
+
+// Device address of dash_scratch on each device, looked up once per device
+// (in host code the array's name is a host-side stand-in, not a device
+// address).
+void* g_scratch[64];
+
+int scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DASH_ERR_NO_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(DASH_ERR_NO_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(dash_scratch));
+    if (e != hipSuccess || !p) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return DASH_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
+                     void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal, int schedule,
+                     float scale, void* workspace, size_t ws_bytes, const dash_bwd_options_t* opts,
+                     void* stream) {
+  return bwd_launch(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale, workspace, ws_bytes, opts,
+                    nullptr, stream);
+}
+
+int dash_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dO,
+                          const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal,
+                          int schedule, float scale, int* status, void* stream) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if ((size_t)B * H * N == 0) return DASH_OK;
+  const size_t need = dash_bwd_workspace_size(B, H, N, d, schedule);
+  if (need == 0) return fail(DASH_ERR_INVALID_ARG, "unknown schedule");
+  if (need > kScratchBytes)
+    return fail(DASH_ERR_UNSUPPORTED, "problem needs " + std::to_string(need) + " bytes of scratch, more than the " +
+                                          std::to_string(kScratchBytes) + " of dash_attn_bwd_noalloc");
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc) return rc;
+  return bwd_launch(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale, ws, kScratchBytes, nullptr,
+                    status, stream);
 }
 
 int dash_bwd_check(void* workspace, void* stream) {

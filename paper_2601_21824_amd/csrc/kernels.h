@@ -63,6 +63,7 @@ struct BwdArgs {
   int poison;
   Geom G;
   hipEvent_t ev_begin, ev_end;  // optional, recorded around bwd_main
+  int* status;      // optional caller-owned device int: bwd_pre writes 0, a wait timeout 1
   unsigned long long* wait_stats;  // optional ordering-wait statistics (see dash_bwd_options_t)
 };
 
