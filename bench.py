@@ -129,7 +129,14 @@ def cpu_baseline(q, k, v, do, causal, flops_per_head):
         if time.perf_counter() - t0 >= 10.0:
             break
     dt = time.perf_counter() - t0
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), model)
+    except OSError:
+        pass
     return {"value": heads * flops_per_head / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
+            "cpu_model": model,
             "sample": f"{heads} full head(s) of the workload in order from (b=0,h=0), fp64 forward recompute "
                       f"+ dQ/dK/dV, {dt:.1f} s; FLOPs counted as 4*N^2*d*2.5 per head (halved for causal)"}
 

@@ -203,6 +203,12 @@ size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule);
  * ws_bytes >= dash_bwd_workspace_size(B,H,N,d,schedule) bytes (256-byte aligned).  The
  * workspace must not be used by another call until this one has finished.
  * A wait timeout is recorded in the workspace; read it with dash_bwd_check.
+ * Shift and Symmetric Shift chains wait on each other in a cycle (Section
+ * 3.1 assumes one KV tile per SM, all running at once): their main kernel is
+ * launched cooperatively, so a grid the device cannot keep resident at once
+ * (e.g. while other work occupies its CUs) is refused at launch with
+ * DASH_ERR_UNSUPPORTED instead of spinning into the wait watchdog.  The other
+ * schedules wait only on chains that started earlier.
  */
 int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO,
                      const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,

@@ -750,47 +750,41 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
 }
 
 template <int D, bool CAUSAL>
-void launch_main_mask(const BwdArgs& a, int grid_main, hipStream_t stream) {
-  const dim3 grid(grid_main), block(256);
-  if (a.G.sched == S_ATOMIC)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeAtomic>), grid, block, 0, stream, a);
-  else if (a.G.sched == S_PARTIALS)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModePartials>), grid, block, 0, stream, a);
-  else if (a.G.sched == S_SPLIT)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeNoDq>), grid, block, 0, stream, a);
-  else if (a.nxcd > 0 && a.wait_stats)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrderedXcd, true>), grid, block, 0, stream, a);
-  else if (a.nxcd > 0)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrderedXcd>), grid, block, 0, stream, a);
-  else if (a.wait_stats)
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered, true>), grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL((bwd_main_kernel<D, CAUSAL, kModeOrdered>), grid, block, 0, stream, a);
+hipError_t launch_main_mask(const BwdArgs& a, int grid, hipStream_t stream) {
+  if (a.G.sched == S_ATOMIC) return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeAtomic>, a, grid, 256, stream);
+  if (a.G.sched == S_PARTIALS) return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModePartials>, a, grid, 256, stream);
+  if (a.G.sched == S_SPLIT) return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeNoDq>, a, grid, 256, stream);
+  if (a.nxcd > 0 && a.wait_stats)
+    return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeOrderedXcd, true>, a, grid, 256, stream);
+  if (a.nxcd > 0) return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeOrderedXcd>, a, grid, 256, stream);
+  if (a.wait_stats) return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeOrdered, true>, a, grid, 256, stream);
+  return launch_main_grid(bwd_main_kernel<D, CAUSAL, kModeOrdered>, a, grid, 256, stream);
 }
 
 template <int D>
-void launch_main(const BwdArgs& a, int grid_main, hipStream_t stream) {
-  if (a.G.causal)
-    launch_main_mask<D, true>(a, grid_main, stream);
-  else
-    launch_main_mask<D, false>(a, grid_main, stream);
+hipError_t launch_main(const BwdArgs& a, int grid_main, hipStream_t stream) {
+  return a.G.causal ? launch_main_mask<D, true>(a, grid_main, stream) : launch_main_mask<D, false>(a, grid_main, stream);
 }
 
 template <int D>
-void launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t stream) {
+hipError_t launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStream_t stream) {
   const bool atomic = a.G.sched == S_ATOMIC;
   hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(256), 0, stream, a, (int)atomic);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
   if constexpr (D == 256)
-    launch_main256(a, grid_main, stream);
+    e = launch_main256(a, grid_main, stream);
   else
-    launch_main<D>(a, grid_main, stream);
+    e = launch_main<D>(a, grid_main, stream);
+  if (e != hipSuccess) return e;
   if (a.ev_end) (void)hipEventRecord(a.ev_end, stream);
   if (atomic) hipLaunchKernelGGL(bwd_post_kernel<D>, dim3(1024), dim3(256), 0, stream, a);
   if constexpr (D <= 128) {
     if (a.G.sched == S_PARTIALS) hipLaunchKernelGGL(bwd_sum_partials_kernel<D>, dim3(4096), dim3(256), 0, stream, a);
     if (a.G.sched == S_SPLIT) (void)launch_dq(a, D, stream);
   }
+  return hipGetLastError();
 }
 
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream) {
@@ -799,13 +793,9 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
   long pre_blocks = (rows * tpr + 255) / 256;
   if (pre_blocks < 1) pre_blocks = 1;
   if (pre_blocks > 65535L * 16) pre_blocks = 65535L * 16;
-  if (d == 64)
-    launch_all<64>(a, pre_blocks, grid_main, stream);
-  else if (d == 128)
-    launch_all<128>(a, pre_blocks, grid_main, stream);
-  else
-    launch_all<256>(a, pre_blocks, grid_main, stream);
-  return hipGetLastError();
+  if (d == 64) return launch_all<64>(a, pre_blocks, grid_main, stream);
+  if (d == 128) return launch_all<128>(a, pre_blocks, grid_main, stream);
+  return launch_all<256>(a, pre_blocks, grid_main, stream);
 }
 
 template <int D>

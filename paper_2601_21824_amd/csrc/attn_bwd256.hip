@@ -431,24 +431,19 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
   if constexpr (STATS) stats_wave_end(wst, a.wait_stats, l);
 }
 
+template <bool CAUSAL>
+hipError_t launch_main256_mask(const BwdArgs& a, int grid, hipStream_t stream) {
+  if (a.G.sched == S_ATOMIC) return launch_main_grid(bwd_main256_kernel<CAUSAL, false, false>, a, grid, NT, stream);
+  if (a.nxcd > 0 && a.wait_stats) return launch_main_grid(bwd_main256_kernel<CAUSAL, true, true, true>, a, grid, NT, stream);
+  if (a.nxcd > 0) return launch_main_grid(bwd_main256_kernel<CAUSAL, true, true>, a, grid, NT, stream);
+  if (a.wait_stats) return launch_main_grid(bwd_main256_kernel<CAUSAL, true, false, true>, a, grid, NT, stream);
+  return launch_main_grid(bwd_main256_kernel<CAUSAL, true, false>, a, grid, NT, stream);
+}
+
 }  // namespace
 
-void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream) {
-  const bool atomic = a.G.sched == S_ATOMIC;
-  const dim3 grid(grid_main), block(NT);
-  if (a.G.causal) {
-    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<true, false, false>), grid, block, 0, stream, a);
-    else if (a.nxcd > 0 && a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<true, true, true, true>), grid, block, 0, stream, a);
-    else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<true, true, true>), grid, block, 0, stream, a);
-    else if (a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<true, true, false, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main256_kernel<true, true, false>), grid, block, 0, stream, a);
-  } else {
-    if (atomic) hipLaunchKernelGGL((bwd_main256_kernel<false, false, false>), grid, block, 0, stream, a);
-    else if (a.nxcd > 0 && a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<false, true, true, true>), grid, block, 0, stream, a);
-    else if (a.nxcd > 0) hipLaunchKernelGGL((bwd_main256_kernel<false, true, true>), grid, block, 0, stream, a);
-    else if (a.wait_stats) hipLaunchKernelGGL((bwd_main256_kernel<false, true, false, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((bwd_main256_kernel<false, true, false>), grid, block, 0, stream, a);
-  }
+hipError_t launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream) {
+  return a.G.causal ? launch_main256_mask<true>(a, grid_main, stream) : launch_main256_mask<false>(a, grid_main, stream);
 }
 
 int bwd_main256_occupancy() {

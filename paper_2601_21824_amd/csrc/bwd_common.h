@@ -173,6 +173,22 @@ __device__ inline void vm_wait_le(int n) {
   else vm_wait<0>();
 }
 
+// Launch a main-kernel instantiation on the persistent grid.  Shift and
+// Symmetric Shift chains wait on each other in a cycle, so every workgroup of
+// their grid must be resident at once: they launch cooperatively, and a grid
+// the device cannot keep resident fails at launch (instead of spinning into
+// the wait watchdog).  The others wait only on earlier tickets.
+template <typename Kernel>
+hipError_t launch_main_grid(Kernel kernel, const BwdArgs& a, int grid, int threads, hipStream_t stream) {
+  if (a.G.sched == S_SHIFT || a.G.sched == S_SYMSHIFT) {
+    BwdArgs copy = a;  // the arguments are copied at launch
+    void* args[] = {&copy};
+    return hipLaunchCooperativeKernel((const void*)kernel, dim3(grid), dim3(threads), args, 0, stream);
+  }
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, stream, a);
+  return hipGetLastError();
+}
+
 // One step of a chain, packed for the LDS step table: 64-row block pb (12
 // bits), KV tile j (9), rank in the block's summation order (10), last (1).
 // kNoStep marks a step whose block or KV tile lies past N.

@@ -88,7 +88,8 @@ __global__ void xcc_probe_kernel(int* out) {
 
 // Number of XCDs if the dispatcher deals workgroups out to them round-robin
 // (what the XCD-local placement relies on to give every XCD its share of a
-// persistent grid), else 0.
+// persistent grid whose size is a multiple of the XCD count), else 0.  The
+// deal may start at any XCD: it continues from the previous dispatch.
 int probe_xcds() {
   constexpr int kWg = 64;
   int* d = nullptr;
@@ -102,7 +103,7 @@ int probe_xcds() {
   for (int i = 0; i < kWg; ++i) n = h[i] + 1 > n ? h[i] + 1 : n;
   if (n < 1 || n > dash::kMaxXcd) return 0;
   for (int i = 0; i < kWg; ++i)
-    if (h[i] != i % n) return 0;
+    if (h[i] != (h[0] + i) % n) return 0;
   return n;
 }
 
@@ -388,6 +389,9 @@ int bwd_launch(const void* q, const void* k, const void* v, const void* o, const
   a.ev_end = timed ? (hipEvent_t)opts->event_main_end : nullptr;
   a.status = status;
   hipError_t e = dash::launch_bwd(a, d, grid, (hipStream_t)stream);
+  if (e == hipErrorCooperativeLaunchTooLarge)
+    return fail(DASH_ERR_UNSUPPORTED, "the device cannot keep every chain of a Shift group (Symmetric Shift: of a head) "
+                                      "resident at once: cooperative launch refused");
   if (e != hipSuccess) return hip_fail(e, "backward launch");
   return DASH_OK;
 }

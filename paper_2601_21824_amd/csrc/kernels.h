@@ -72,7 +72,7 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 hipError_t launch_dq(const BwdArgs& a, int d, hipStream_t stream);  // SPLIT's dQ pass (attn_dq.hip)
 int bwd_main_occupancy(int d);
 // head dim 256 (attn_bwd256.hip)
-void launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream);
+hipError_t launch_main256(const BwdArgs& a, int grid_main, hipStream_t stream);
 int bwd_main256_occupancy();
 // measured MFMA throughput (mfma_peak.hip): grid workgroups of 4 waves
 void launch_mfma_peak(int grid, int iters, float* sink, hipStream_t stream);
