@@ -172,20 +172,28 @@ class Deadlock(RuntimeError):
     pass
 
 
-def simulate(schedules, n_workers: int, c, r):
+def simulate(schedules, n_workers: int, c, r, chain_major: bool = False):
     """Critical path of the DAG model of Section 3.1, by list scheduling.
 
-    schedules: one Schedule per head, dispatched head-major, chain by chain, to
-    n_workers identical SMs; a free SM takes the next chain.  Every task is a
-    compute phase of length c followed by a reduction phase of length r; a
-    chain runs its tasks back to back.  A reduction into dQ tile i of a head
-    may start only after the reduction of the previous KV tile in that tile's
-    accumulation order (a zero-weight dependency edge).  Returns the makespan.
+    schedules: one Schedule per head, dispatched to n_workers identical SMs
+    head-major (all chains of head 0, then head 1, ...) or, with chain_major,
+    chain w of every head before chain w+1; a free SM takes the next chain.
+    Every task is a compute phase of length c followed by a reduction phase of
+    length r; a chain runs its tasks back to back.  A reduction into dQ tile i
+    of a head may start only after the reduction of the previous KV tile in
+    that tile's accumulation order (a zero-weight dependency edge).  Returns
+    the makespan.
     """
     queue = []  # chains in dispatch order: (head, chain)
-    for h, s in enumerate(schedules):
-        for w in range(len(s.chains)):
-            queue.append((h, w))
+    if chain_major:
+        for w in range(max(len(s.chains) for s in schedules)):
+            for h, s in enumerate(schedules):
+                if w < len(s.chains):
+                    queue.append((h, w))
+    else:
+        for h, s in enumerate(schedules):
+            for w in range(len(s.chains)):
+                queue.append((h, w))
     pred = {}  # (h, i, j) -> (h, i, j_prev) or None
     for h, s in enumerate(schedules):
         for i, js in s.order.items():
