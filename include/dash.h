@@ -53,9 +53,10 @@ typedef enum {
   /* Symmetric Shift (Section 3.4, causal masks): KV tiles j and T-1-j share a
      workgroup; two-phase fold.  Causal mask only. */
   DASH_SCHED_SYMSHIFT = 4,
-  /* SHIFT for full masks, DESCENDING for causal masks (the paper's choice at
-     d >= 128, Section 4.3; on this GPU it also beats SYMSHIFT at d = 64 and
-     on long sequences at every d). */
+  /* The deterministic schedule the DAG model of Section 3.1, calibrated on
+     MI355X, predicts to be fastest for the call's (B, H, N, d, mask) on the
+     current device: SHIFT, NAIVE or DESCENDING for a full mask, DESCENDING,
+     NAIVE or SYMSHIFT for a causal mask (see dash_auto_schedule). */
   DASH_SCHED_AUTO = 5,
   /* Comparison point (related work, "Deterministic Implementations"): every
      KV tile stores its dQ partial in its own fp32 buffer, no ordering waits;
@@ -240,8 +241,44 @@ int dash_attn_bwd_noalloc(const void* q, const void* k, const void* v, const voi
    that used `workspace` hit a wait timeout, DASH_OK otherwise. */
 int dash_bwd_check(void* workspace, void* stream);
 
-/* The concrete schedule DASH_SCHED_AUTO / SHIFT resolve to for (d, causal). */
+/* The concrete schedule SHIFT resolves to for the mask (SYMSHIFT when
+   causal); for DASH_SCHED_AUTO, which depends on B, H and N as well, the
+   mask's default when no shape is known (SHIFT for a full mask, DESCENDING for
+   a causal one; a backward call picks with dash_auto_schedule instead).
+   Other schedules are returned unchanged. */
 int dash_resolve_schedule(int schedule, int d, int causal);
+
+/* DASH_SCHED_AUTO's choice for a backward of B x H heads of length N at head
+   dim d (Section 3.1's DAG model).  Every candidate deterministic schedule is
+   simulated as the kernels run it -- its chains of 64-row block steps in
+   step-table order, tickets in the library's order, a free workgroup taking
+   the next ticket, each block's reductions in its summation order -- with
+   the block-step time measured for that schedule on MI355X at this (d, mask)
+   and interpolated in N; the shortest predicted makespan wins (ties: SHIFT /
+   DESCENDING).  Candidates whose co-running chains exceed the workgroups are
+   left out.  `workers` is the number of resident workgroups (0: the current
+   device's, which needs the device).  *schedule receives the choice and
+   *predicted_ms (if not NULL) the predicted makespan in milliseconds (-1 when
+   nothing was calibrated for this d and mask, or the problem is empty).  The
+   first call for a shape simulates (at most enough heads to fill the
+   workgroups three times; milliseconds of host time), later ones read a
+   per-process cache. */
+int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int* schedule, double* predicted_ms);
+
+/* Section 3.1's DAG model of a backward call with explicit costs: every block
+   step (64 query rows against one KV tile, as the kernels step) computes for
+   c and then reduces for r; a reduction starts once the block's previous
+   contributor in the summation order has reduced.  `schedule` is NAIVE,
+   DESCENDING, SHIFT or SYMSHIFT (SHIFT with causal != 0 is SYMSHIFT);
+   ticket_order as in dash_bwd_options_t (AUTO: the library's order for
+   `workers` resident workgroups).  max_heads = 0 simulates all B*H heads
+   (host time grows with B*H*N^2); max_heads > 0 simulates at most that many
+   and scales the makespan by B*H / max_heads (dash_auto_schedule uses
+   ceil(3 * workers / chains per head)).  *makespan receives the critical
+   path in the units of c and r.  DASH_ERR_UNSUPPORTED when chains that must
+   run together exceed `workers` (no chain can finish); no device needed. */
+int dash_model_makespan(int schedule, int B, int H, int N, int d, int causal, int workers, int ticket_order,
+                        int max_heads, double c, double r, double* makespan);
 
 /* The placement (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD) that
    dash_attn_bwd_ex picks with placement AUTO for this problem on the current

@@ -28,7 +28,8 @@ DASH_PLACEMENT_AUTO, DASH_PLACEMENT_GLOBAL, DASH_PLACEMENT_XCD = 0, 1, 2
 # every symbol include/dash.h declares
 EXPORTS = ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_bwd_workspace_size",
            "dash_attn_bwd_ex", "dash_attn_bwd_noalloc", "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table",
-           "dash_bwd_placement", "dash_mfma_peak", "dash_last_error", "dash_release_workspace")
+           "dash_bwd_placement", "dash_mfma_peak", "dash_last_error", "dash_release_workspace",
+           "dash_auto_schedule", "dash_model_makespan")
 
 
 class DashError(RuntimeError):
@@ -71,11 +72,14 @@ def load():
         lib.dash_schedule_table.argtypes = [ci] * 5 + [ip] * 5
         lib.dash_bwd_placement.argtypes = [ci] * 6
         lib.dash_mfma_peak.argtypes = [ci, ctypes.POINTER(ctypes.c_double)]
+        dp = ctypes.POINTER(ctypes.c_double)
+        lib.dash_auto_schedule.argtypes = [ci] * 6 + [ip, dp]
+        lib.dash_model_makespan.argtypes = [ci] * 9 + [ctypes.c_double, ctypes.c_double, dp]
         lib.dash_last_error.restype = ctypes.c_char_p
         lib.dash_release_workspace.restype = None
         for f in ("dash_attn_fwd", "dash_attn_fwd_ex", "dash_attn_bwd", "dash_attn_bwd_ex", "dash_attn_bwd_noalloc",
                   "dash_bwd_check", "dash_resolve_schedule", "dash_schedule_table", "dash_bwd_placement",
-                  "dash_mfma_peak"):
+                  "dash_mfma_peak", "dash_auto_schedule", "dash_model_makespan"):
             getattr(lib, f).restype = ci
         _lib = lib
     return _lib
@@ -126,6 +130,22 @@ def dash_release_workspace():
 
 def dash_resolve_schedule(schedule, d: int, causal: bool) -> int:
     return load().dash_resolve_schedule(_sched(schedule), d, int(causal))
+
+
+def dash_auto_schedule(B: int, H: int, N: int, d: int, causal: bool, workers: int = 0):
+    """(schedule, predicted ms) that DASH_SCHED_AUTO runs for this shape."""
+    s, ms = ctypes.c_int(), ctypes.c_double()
+    _check(load().dash_auto_schedule(B, H, N, d, int(causal), workers, ctypes.byref(s), ctypes.byref(ms)))
+    return s.value, ms.value
+
+
+def dash_model_makespan(schedule, B: int, H: int, N: int, d: int, causal: bool, workers: int, c: float, r: float,
+                        ticket_order: int = DASH_TICKETS_AUTO, max_heads: int = 0) -> float:
+    """Makespan of the DAG model with block-step costs c (compute) and r (reduction)."""
+    m = ctypes.c_double()
+    _check(load().dash_model_makespan(_sched(schedule), B, H, N, d, int(causal), workers, ticket_order,
+                                      max_heads, c, r, ctypes.byref(m)))
+    return m.value
 
 
 def dash_bwd_workspace_size(B: int, H: int, N: int, d: int, schedule="shift") -> int:

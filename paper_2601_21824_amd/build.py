@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdash.so")
 SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd256.hip", "attn_dq.hip", "mfma_peak.hip", "dash_api.hip"]
-HEADERS = ["common.h", "kernels.h", "schedule.h"]
+HEADERS = ["common.h", "kernels.h", "schedule.h", "bwd_common.h", "lds_layout.h", "dag_model.h", "model_calibration.h"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -5,11 +5,15 @@
 
 #include <cmath>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 
+#include "dag_model.h"
 #include "dash.h"
 #include "kernels.h"
+#include "model_calibration.h"
 #include "schedule.h"
 
 namespace {
@@ -227,6 +231,129 @@ int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, 
   return DASH_OK;
 }
 
+// DASH_TICKETS_AUTO's ticket order.  Chain-major while a head has fewer
+// chains than resident workgroups: head-major would put all of a head's
+// chains on the GPU at once, and with naive / Descending every one of them
+// waits out the whole pipeline fill of the head (chain j's first turn comes j
+// steps late); chain-major keeps few chains per head in flight and starts the
+// longest first.  The variants without ordering waits only gain the
+// longest-first balance, so they go chain-major under a causal mask only.
+// Once one head's chains fill the GPU, head-major keeps the resident
+// workgroups on one head's Q / dO and wins.  (Measured over d = 64 / 128 /
+// 256 and both masks.)  Under XCD-local placement an XCD's queue holds several
+// heads whose chains outnumber its resident workgroups: chain-major keeps the
+// naive pipeline fill short there as well, and for Descending except with a
+// causal mask at d = 128, where its chains all start at the last Q tile and
+// head-major measured better.  Shift and Symmetric Shift are head-major.
+bool auto_chain_major(int sched, int causal, int d, long chains, long resident, bool xcd) {
+  if (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT) return false;
+  const bool waits = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING;
+  if (xcd) return sched == DASH_SCHED_NAIVE || (sched == DASH_SCHED_DESCENDING && (!causal || d < 128));
+  return chains < resident && (waits || causal);
+}
+
+// ---- the DAG model (Section 3.1) and DASH_SCHED_AUTO
+
+// Measured time of one block step of `sched` at (d, mask) for `heads` heads of
+// length N, interpolated log-linearly between the calibrated shapes (first in
+// the number of heads at the two calibrated lengths around N, then in N) and
+// held constant beyond them; < 0 when nothing was calibrated at (d, mask).
+double step_us_at(int d, int causal, int sched, int n, long heads) {
+  double h0 = -1, u0 = 0, h1 = -1, u1 = 0;  // nearest calibrated head counts below / above
+  for (const dash::StepCost& e : dash::kStepCosts) {
+    if (e.d != d || e.causal != causal || e.sched != sched || e.n != n) continue;
+    if (e.heads <= heads && (h0 < 0 || e.heads > h0)) h0 = e.heads, u0 = e.us;
+    if (e.heads >= heads && (h1 < 0 || e.heads < h1)) h1 = e.heads, u1 = e.us;
+  }
+  if (h0 < 0) return u1;
+  if (h1 < 0 || h1 == h0) return u0;
+  const double f = std::log2((double)heads / h0) / std::log2(h1 / h0);
+  return u0 + f * (u1 - u0);
+}
+
+double step_us(int d, int causal, int sched, int N, long heads) {
+  double n0 = -1, n1 = -1;  // nearest calibrated lengths at or below / at or above N
+  for (const dash::StepCost& e : dash::kStepCosts) {
+    if (e.d != d || e.causal != causal || e.sched != sched || e.n <= 0) continue;
+    if (e.n <= N && (n0 < 0 || e.n > n0)) n0 = e.n;
+    if (e.n >= N && (n1 < 0 || e.n < n1)) n1 = e.n;
+  }
+  if (n0 < 0 && n1 < 0) return -1.0;
+  if (n0 < 0) return step_us_at(d, causal, sched, (int)n1, heads);
+  if (n1 < 0 || n1 == n0) return step_us_at(d, causal, sched, (int)n0, heads);
+  const double u0 = step_us_at(d, causal, sched, (int)n0, heads), u1 = step_us_at(d, causal, sched, (int)n1, heads);
+  const double f = std::log2((double)N / n0) / std::log2(n1 / n0);
+  return u0 + f * (u1 - u0);
+}
+
+// Makespan of B*H heads on `workers` workgroups with compute c and reduction
+// r per block step; `head_cap` > 0 simulates at most that many heads and
+// scales the result to B*H.  Returns < 0 if the model deadlocks.
+double model_makespan(int sched, int B, int H, int N, int d, int causal, long workers, int tickets, double c,
+                      double r, long head_cap) {
+  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  G.chain_major = tickets != DASH_TICKETS_AUTO ? tickets == DASH_TICKETS_CHAIN_MAJOR
+                                               : auto_chain_major(sched, causal, d, G.chains, workers, false);
+  const dash::HeadDag hd = dash::build_head_dag(G, N);
+  const long heads = (long)B * H;
+  const long sim = head_cap > 0 && heads > head_cap ? head_cap : heads;
+  const double m = dash::simulate_dag(G, hd, (int)sim, (int)workers, c, r);
+  return m < 0 ? m : m * (double)heads / (double)sim;
+}
+
+// Heads simulated for DASH_SCHED_AUTO: enough to fill the workgroups three times.
+long model_head_cap(long chains, long resident) {
+  const long cap = (3 * resident + chains - 1) / chains;
+  return cap > 0 ? cap : 1;
+}
+
+// DASH_SCHED_AUTO: the deterministic schedule with the shortest makespan the
+// calibrated model predicts for this shape (ties: the mask's default, Shift /
+// Descending).  Candidates the device cannot run (a Shift group or a head's
+// Symmetric Shift chains beyond the resident workgroups) are left out.  A
+// shape is simulated once per process; at most enough heads to fill the
+// workgroups three times are simulated.
+std::mutex g_auto_mu;
+std::map<std::tuple<int, int, int, int, int, long>, std::pair<int, double>> g_auto;
+
+int auto_pick(int B, int H, int N, int d, int causal, long resident, int* sched, double* ms) {
+  const auto key = std::make_tuple(B, H, N, d, causal, resident);
+  {
+    std::lock_guard<std::mutex> lk(g_auto_mu);
+    auto it = g_auto.find(key);
+    if (it != g_auto.end()) {
+      *sched = it->second.first;
+      if (ms) *ms = it->second.second;
+      return DASH_OK;
+    }
+  }
+  const int cand[3] = {causal ? DASH_SCHED_DESCENDING : DASH_SCHED_SHIFT, DASH_SCHED_NAIVE,
+                       causal ? DASH_SCHED_SYMSHIFT : DASH_SCHED_DESCENDING};
+  int best = cand[0];
+  double best_us = -1.0;
+  if ((long)B * H * N > 0 && resident > 0) {
+    for (int s : cand) {
+      const dash::Geom G = dash::make_geom(s, causal, N, d);
+      const long together = s == DASH_SCHED_SHIFT ? G.grp : s == DASH_SCHED_SYMSHIFT ? G.chains : 1;
+      if (together > resident) continue;
+      const double us = step_us(d, causal, s, N, (long)B * H);
+      if (us <= 0) continue;
+      const long cap = model_head_cap(G.chains, resident);
+      const double m = model_makespan(s, B, H, N, d, causal, resident, DASH_TICKETS_AUTO,
+                                      dash::kModelComputeShare * us, (1.0 - dash::kModelComputeShare) * us,
+                                      cap);
+      if (m < 0) continue;
+      if (best_us < 0 || m < best_us * (1.0 - 1e-9)) best = s, best_us = m;
+    }
+  }
+  const double best_ms = best_us < 0 ? -1.0 : best_us * 1e-3;
+  std::lock_guard<std::mutex> lk(g_auto_mu);
+  g_auto[key] = {best, best_ms};
+  *sched = best;
+  if (ms) *ms = best_ms;
+  return DASH_OK;
+}
+
 void* g_ws = nullptr;
 size_t g_ws_bytes = 0;
 std::mutex g_ws_mu;
@@ -293,11 +420,14 @@ int bwd_launch(const void* q, const void* k, const void* v, const void* o, const
   const int placement = opts ? opts->placement : DASH_PLACEMENT_AUTO;
   if (placement < DASH_PLACEMENT_AUTO || placement > DASH_PLACEMENT_XCD)
     return fail(DASH_ERR_INVALID_ARG, "unknown placement");
-  const int sched = resolve(schedule, d, causal);
-  if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
-    return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
   DeviceInfo di;
   if ((rc = device_info(&di, placement == DASH_PLACEMENT_XCD))) return rc;
+  int sched = resolve(schedule, d, causal);
+  if (schedule == DASH_SCHED_AUTO &&
+      (rc = auto_pick(B, H, N, d, causal, (long)occupancy(di, d) * di.cus, &sched, nullptr)))
+    return rc;
+  if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
+    return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
 
   dash::Geom G = dash::make_geom(sched, causal, N, d);
   bool xcd = false;
@@ -307,29 +437,8 @@ int bwd_launch(const void* q, const void* k, const void* v, const void* o, const
   const int nq = xcd ? di.nxcd : 1;  // ticket queues; workgroup i serves queue i % nq
   // workgroups one queue keeps resident
   const long resident = (long)occupancy(di, d) * di.cus / nq;
-  if (tickets != DASH_TICKETS_AUTO) {
-    G.chain_major = tickets == DASH_TICKETS_CHAIN_MAJOR;
-  } else if (sched != DASH_SCHED_SHIFT && sched != DASH_SCHED_SYMSHIFT) {
-    // Chain-major while a head has fewer chains than resident workgroups:
-    // head-major would put all of a head's chains on the GPU at once, and
-    // with naive / Descending every one of them waits out the whole pipeline
-    // fill of the head (chain j's first turn comes j steps late); chain-major
-    // keeps few chains per head in flight and starts the longest first.  The
-    // variants without ordering waits only gain the longest-first balance, so
-    // they go chain-major under a causal mask only.  Once one head's chains
-    // fill the GPU, head-major keeps the resident workgroups on one head's
-    // Q / dO and wins.  (Measured over d = 64 / 128 / 256 and both masks.)
-    // Under XCD-local placement an XCD's queue holds several heads whose
-    // chains outnumber its resident workgroups: chain-major keeps the naive
-    // pipeline fill short there as well, and for Descending except with a
-    // causal mask at d = 128, where its chains all start at the last Q tile
-    // and head-major measured better.
-    const bool waits = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING;
-    if (xcd)
-      G.chain_major = sched == DASH_SCHED_NAIVE || (sched == DASH_SCHED_DESCENDING && (!causal || d < 128));
-    else
-      G.chain_major = (long)G.chains < resident && (waits || causal);
-  }
+  G.chain_major = tickets != DASH_TICKETS_AUTO ? tickets == DASH_TICKETS_CHAIN_MAJOR
+                                                : auto_chain_major(sched, causal, d, G.chains, resident, xcd);
   // Shift-type chains wait on each other in a cycle: every chain of a Shift
   // group (Symmetric Shift: of a head) must be able to run at once.  Naive and
   // Descending chains only wait on chains with lower work tickets, which the
@@ -479,6 +588,42 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
                         g_ws_bytes, nullptr, nullptr);
   if (rc) return rc;
   return dash_bwd_check(g_ws, nullptr);
+}
+
+int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int* schedule, double* predicted_ms) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if (!schedule) return fail(DASH_ERR_INVALID_ARG, "schedule is NULL");
+  if (workers < 0) return fail(DASH_ERR_INVALID_ARG, "workers < 0");
+  long resident = workers;
+  if (workers == 0) {
+    DeviceInfo di;
+    if ((rc = device_info(&di))) return rc;
+    resident = (long)occupancy(di, d) * di.cus;
+  }
+  return auto_pick(B, H, N, d, causal ? 1 : 0, resident, schedule, predicted_ms);
+}
+
+int dash_model_makespan(int schedule, int B, int H, int N, int d, int causal, int workers, int ticket_order,
+                        int max_heads, double c, double r, double* makespan) {
+  int rc = check_shape(B, H, N, d);
+  if (rc) return rc;
+  if ((rc = check_schedule(schedule, causal))) return rc;
+  if (schedule != DASH_SCHED_NAIVE && schedule != DASH_SCHED_DESCENDING && schedule != DASH_SCHED_SHIFT &&
+      schedule != DASH_SCHED_SYMSHIFT)
+    return fail(DASH_ERR_INVALID_ARG, "the model covers the ordered schedules (naive, descending, shift, symshift)");
+  if (!makespan) return fail(DASH_ERR_INVALID_ARG, "makespan is NULL");
+  if (workers <= 0) return fail(DASH_ERR_INVALID_ARG, "workers must be > 0");
+  if (ticket_order < DASH_TICKETS_AUTO || ticket_order > DASH_TICKETS_CHAIN_MAJOR)
+    return fail(DASH_ERR_INVALID_ARG, "unknown ticket_order");
+  if (max_heads < 0) return fail(DASH_ERR_INVALID_ARG, "max_heads < 0");
+  if (!(c >= 0) || !(r >= 0) || !std::isfinite(c) || !std::isfinite(r))
+    return fail(DASH_ERR_INVALID_ARG, "c and r must be finite and >= 0");
+  const int sched = resolve(schedule, d, causal);
+  const double m = model_makespan(sched, B, H, N, d, causal ? 1 : 0, workers, ticket_order, c, r, max_heads);
+  if (m < 0) return fail(DASH_ERR_UNSUPPORTED, "the chains that must run together exceed the workgroups: no chain finishes");
+  *makespan = m;
+  return DASH_OK;
 }
 
 int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule) {

@@ -320,6 +320,39 @@ def test_placement(case):
         assert e.value.code == dash.DASH_ERR_INVALID_ARG
 
 
+AUTO_CASES = [  # shapes at which the model picks each of the four schedules on MI355X
+    (1, 32, 512, 128, False),
+    (1, 2, 8192, 128, False),
+    (1, 8, 2048, 128, True),
+    (1, 128, 4096, 128, True),
+    (1, 16, 1024, 64, True),
+    (2, 3, 200, 64, True),
+]
+
+
+@pytest.mark.parametrize("case", AUTO_CASES, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}"
+                                                  for c in AUTO_CASES])
+def test_auto_runs_the_model_choice(case):
+    """DASH_SCHED_AUTO runs the schedule dash_auto_schedule reports for the
+    device (the DAG model's pick): the same bits as that schedule called by
+    name, twice; the pick is one of the mask's deterministic schedules."""
+    B, H, N, d, causal = case
+    pick, ms = dash.dash_auto_schedule(B, H, N, d, causal)
+    allowed = (dash.DASH_SCHED_DESCENDING, dash.DASH_SCHED_NAIVE, dash.DASH_SCHED_SYMSHIFT) if causal else \
+        (dash.DASH_SCHED_SHIFT, dash.DASH_SCHED_NAIVE, dash.DASH_SCHED_DESCENDING)
+    assert pick in allowed and ms > 0
+    print(f"\n[auto] {case} -> {pick} ({ms:.3f} ms predicted)", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=31)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    ws = dash.new_workspace(B, H, N, d, "auto")
+    ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, pick, workspace=ws)
+    for _ in range(2):
+        got = run_bwd(qg, kg, vg, og, dog, lseg, causal, "auto", workspace=ws)
+        assert dash.dash_bwd_check(ws) == dash.DASH_OK
+        for a_, b_ in zip(got, ref):
+            assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
+
+
 @pytest.mark.parametrize("d", [256])
 def test_shift_groups_order_and_minimal_grid(d):
     """N = 32768 gives 512 KV tiles per head at d = 256 (64-row KV tiles), so
