@@ -89,7 +89,7 @@ def ordering_wait(dash, tensors, causal, sched, B, H, N, d):
     if dash.dash_bwd_check(ws) != dash.DASH_OK:
         raise RuntimeError(f"{sched}: ordering wait timed out (instrumented call)")
     late, wait_ticks, wave_ticks = (int(x) for x in stats.cpu())
-    tab = dash.dash_schedule_table(sched, N, d, causal)
+    tab = dash.dash_schedule_table(sched, N, d, causal, heads=B * H)
     wave_steps = 4 * B * H * int(tab["chain_len"].sum()) * (tab["br"] // 64)  # 64-row steps, 4 waves
     return {"stall_frac": round(wait_ticks / wave_ticks, 4) if wave_ticks > 0 else None,
             "late_wave_steps": late, "wave_steps": wave_steps,

@@ -95,8 +95,7 @@ typedef struct {
   /* DASH_FLAG_* bits */
   int flags;
   /* If non-NULL: int32 [B*H][ceil(N/64)][T_c], T_c = ceil(N/bc) KV tiles of
-     bc rows (bc = 128 for d <= 128, 64 for d = 256; geometry[4] of
-     dash_schedule_table).  The workgroup that adds its partial to 64-row dQ
+     bc rows (geometry[4] of dash_schedule_table for the call's B*H heads).  The workgroup that adds its partial to 64-row dQ
      block p with order position r writes its KV-tile index at [bh][p][r]
      (ordering witness). */
   int32_t* witness;
@@ -296,10 +295,13 @@ int dash_mfma_peak(int iters, double* tflops);
 
 /*
  * Host-side view of the schedule the kernels follow (no GPU needed).  For one
- * head of length N at head dim d: T_r scheduling Q tiles of br rows and T_c
- * KV tiles of bc rows (bc = 128 for d <= 128, 64 for d = 256), under
- * `placement` (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD; only Shift's
- * groups depend on it).  Writes, when the pointer is non-NULL:
+ * head of length N at head dim d, in a call of `heads` = B*H heads: T_r
+ * scheduling Q tiles of br rows and T_c KV tiles of bc rows (bc = 128 at
+ * d = 128 and 64 at d = 256; at d = 64, 256 when the call has at least 256 KV
+ * tiles of 256 rows over all heads (causal: 1024 and N >= 2048), else 128 --
+ * so the summation order depends on the call's number of heads at d = 64),
+ * under `placement` (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD; only
+ * Shift's groups depend on it).  Writes, when the pointer is non-NULL:
  *   geometry[6]            = {T_r, T_c, br, number of workgroup chains per
  *                             head, bc, chains per Shift group (the chains
  *                             that must run at the same time; = chains for
@@ -312,7 +314,7 @@ int dash_mfma_peak(int iters, double* tflops);
  *                            order (-1 when they do not interact)
  * Returns a dash_status_t.
  */
-int dash_schedule_table(int schedule, int N, int d, int causal, int placement, int* geometry, int* chain_len,
+int dash_schedule_table(int schedule, int heads, int N, int d, int causal, int placement, int* geometry, int* chain_len,
                         int* task_kv, int* task_q, int* rank);
 
 const char* dash_last_error(void);

@@ -69,7 +69,7 @@ def load():
         lib.dash_bwd_workspace_size.restype = sz
         lib.dash_bwd_check.argtypes = [vp, vp]
         lib.dash_resolve_schedule.argtypes = [ci] * 3
-        lib.dash_schedule_table.argtypes = [ci] * 5 + [ip] * 5
+        lib.dash_schedule_table.argtypes = [ci] * 6 + [ip] * 5
         lib.dash_bwd_placement.argtypes = [ci] * 6
         lib.dash_mfma_peak.argtypes = [ci, ctypes.POINTER(ctypes.c_double)]
         dp = ctypes.POINTER(ctypes.c_double)
@@ -225,11 +225,12 @@ def dash_mfma_peak(iters: int = 0) -> float:
     return out.value
 
 
-def dash_schedule_table(schedule, N: int, d: int, causal: bool, placement=DASH_PLACEMENT_GLOBAL) -> dict:
-    """The schedule the kernels follow for one head under ``placement`` (host computation)."""
+def dash_schedule_table(schedule, N: int, d: int, causal: bool, placement=DASH_PLACEMENT_GLOBAL, heads: int = 1) -> dict:
+    """The schedule the kernels follow for one head of a call of ``heads`` (= B*H)
+    heads under ``placement`` (host computation)."""
     lib = load()
     geo = (ctypes.c_int * 6)()
-    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), placement, geo, None, None, None, None))
+    _check(lib.dash_schedule_table(_sched(schedule), heads, N, d, int(causal), placement, geo, None, None, None, None))
     t_r, t_c, br, chains, bc, grp = list(geo)
     cap = t_r + 1
     chain_len = np.zeros(chains, np.int32)
@@ -237,7 +238,7 @@ def dash_schedule_table(schedule, N: int, d: int, causal: bool, placement=DASH_P
     task_q = np.full(chains * cap, -1, np.int32)
     rank = np.zeros(t_r * t_c, np.int32)
     p = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
-    _check(lib.dash_schedule_table(_sched(schedule), N, d, int(causal), placement, geo, p(chain_len), p(task_kv),
+    _check(lib.dash_schedule_table(_sched(schedule), heads, N, d, int(causal), placement, geo, p(chain_len), p(task_kv),
                                    p(task_q), p(rank)))
     return dict(t_r=t_r, t_c=t_c, br=br, chains=chains, bc=bc, group=grp, chain_len=chain_len,
                 task_kv=task_kv.reshape(chains, cap), task_q=task_q.reshape(chains, cap),

@@ -10,7 +10,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdash.so")
-SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd256.hip", "attn_dq.hip", "mfma_peak.hip", "dash_api.hip"]
+SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd64w.hip", "attn_bwd256.hip", "attn_dq.hip", "mfma_peak.hip",
+           "dash_api.hip"]
 HEADERS = ["common.h", "kernels.h", "schedule.h", "bwd_common.h", "lds_layout.h", "dag_model.h", "model_calibration.h"]
 
 HIPCC_FLAGS = [

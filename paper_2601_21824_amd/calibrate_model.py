@@ -51,7 +51,7 @@ def main(path=os.path.join(HERE, "model_grid.jsonl")):
         for name, sched in ORDERED.items():
             if name not in r:
                 continue
-            chains = b.dash_schedule_table(sched, N, d, causal)["chains"]
+            chains = b.dash_schedule_table(sched, N, d, causal, heads=B * H)["chains"]
             cap = max(1, -(-3 * WORKERS // chains))
             unit = b.dash_model_makespan(sched, B, H, N, d, causal, WORKERS, COMPUTE_SHARE, 1.0 - COMPUTE_SHARE,
                                          max_heads=cap)

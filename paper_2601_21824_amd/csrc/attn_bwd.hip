@@ -3,7 +3,9 @@
 // bwd_pre  : D = rowsum(dO o O) per query row in fp32 (Algorithm 1, the
 //            preprocessing kernel); resets the ordering counters, the work
 //            ticket and the error flag (and dQacc for the atomic variant).
-// bwd_main : one KV tile of 128 rows per work item (d = 64 and 128), 4 waves;
+// bwd_main : one KV tile of 128 rows per work item (d = 128, and d = 64 where
+//            its tiles are 128 rows; 256-row d = 64 tiles run in
+//            attn_bwd64w.hip, d = 256 in attn_bwd256.hip), 4 waves;
 //            wave w owns KV rows [32w, 32w+32) of the tile and keeps K, V, K^T
 //            operands and the dK, dV accumulators in registers for the whole
 //            chain.  For every
@@ -775,6 +777,8 @@ hipError_t launch_all(const BwdArgs& a, long pre_blocks, int grid_main, hipStrea
   if (a.ev_begin) (void)hipEventRecord(a.ev_begin, stream);
   if constexpr (D == 256)
     e = launch_main256(a, grid_main, stream);
+  else if (D == 64 && a.G.bc == 256)
+    e = launch_main64w(a, grid_main, stream);
   else
     e = launch_main<D>(a, grid_main, stream);
   if (e != hipSuccess) return e;
@@ -820,7 +824,11 @@ int main_occupancy() {
 }
 
 int bwd_main_occupancy(int d) {
-  return d == 64 ? main_occupancy<64>() : d == 128 ? main_occupancy<128>() : bwd_main256_occupancy();
+  if (d == 64) {
+    const int a = main_occupancy<64>(), b = bwd_main64w_occupancy();
+    return a < b ? a : b;
+  }
+  return d == 128 ? main_occupancy<128>() : bwd_main256_occupancy();
 }
 
 }  // namespace dash

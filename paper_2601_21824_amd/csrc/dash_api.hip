@@ -45,7 +45,8 @@ Layout layout(int B, int H, int N, int d, int sched) {
   Layout L;
   const size_t bh = (size_t)B * H;
   const size_t nblk = ((size_t)N + dash::kBlockRows - 1) / dash::kBlockRows;
-  const size_t bc = dash::kv_tile_rows(d);
+  const int bc_f = dash::kv_tile_rows(d, 0, N, (long)bh), bc_c = dash::kv_tile_rows(d, 1, N, (long)bh);
+  const size_t bc = (size_t)(bc_f < bc_c ? bc_f : bc_c);  // PARTIALS: the more tiles of either mask
   const size_t copies = sched == DASH_SCHED_PARTIALS ? ((size_t)N + bc - 1) / bc : 1;
   size_t off = 0;
   L.ctrl = off;
@@ -62,8 +63,8 @@ Layout layout(int B, int H, int N, int d, int sched) {
   // to even), each its length and at most (T_r + 1) * nsub steps (full mask:
   // 64-row Q tiles; causal: Symmetric Shift's padded T_r + 1 tasks); then the
   // ticket order
-  const dash::Geom G = dash::make_geom(dash::S_SHIFT, 0, N, d);
-  const dash::Geom Gc = dash::make_geom(dash::S_SYMSHIFT, 1, N, d);
+  const dash::Geom G = dash::make_geom(dash::S_SHIFT, 0, N, d, (long)bh);
+  const dash::Geom Gc = dash::make_geom(dash::S_SYMSHIFT, 1, N, d, (long)bh);
   const int cap_f = (G.t_r + 1) * G.nsub, cap_c = (Gc.t_r + 1) * Gc.nsub;
   L.step_cap = 1 + (cap_f > cap_c ? cap_f : cap_c);
   const size_t chains = (size_t)(G.t_c > Gc.t_c ? G.t_c : Gc.t_c) + 1;
@@ -211,7 +212,7 @@ int occupancy(const DeviceInfo& di, int d) { return d == 64 ? di.occ64 : d == 12
 // a caller's workgroup cap leaves every XCD those chains -- except that a cap
 // never changes the summation order: where the placement decides Shift's
 // groups, a cap too small for XCD placement is rejected instead.
-int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, int want, bool* xcd) {
+int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, long heads, int want, bool* xcd) {
   *xcd = false;
   if (want != DASH_PLACEMENT_XCD) return DASH_OK;
   // Automatic placement is global: with the accumulator read and written
@@ -220,7 +221,7 @@ int choose_placement(const DeviceInfo& di, int sched, int causal, int N, int d, 
   // it caps a Shift group at the chains one XCD keeps resident.
   const bool ordered = sched == DASH_SCHED_NAIVE || sched == DASH_SCHED_DESCENDING || sched == DASH_SCHED_SHIFT ||
                        sched == DASH_SCHED_SYMSHIFT;
-  dash::Geom Gx = dash::make_geom(sched, causal, N, d);
+  dash::Geom Gx = dash::make_geom(sched, causal, N, d, heads);
   dash::place_on_xcds(Gx);
   const long per_xcd = di.nxcd > 0 ? (long)occupancy(di, d) * di.cus / di.nxcd : 0;
   const long together = sched == DASH_SCHED_SHIFT ? Gx.grp : sched == DASH_SCHED_SYMSHIFT ? Gx.chains : 1;
@@ -291,7 +292,7 @@ double step_us(int d, int causal, int sched, int N, long heads) {
 // scales the result to B*H.  Returns < 0 if the model deadlocks.
 double model_makespan(int sched, int B, int H, int N, int d, int causal, long workers, int tickets, double c,
                       double r, long head_cap) {
-  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  dash::Geom G = dash::make_geom(sched, causal, N, d, (long)B * H);
   G.chain_major = tickets != DASH_TICKETS_AUTO ? tickets == DASH_TICKETS_CHAIN_MAJOR
                                                : auto_chain_major(sched, causal, d, G.chains, workers, false);
   const dash::HeadDag hd = dash::build_head_dag(G, N);
@@ -333,7 +334,7 @@ int auto_pick(int B, int H, int N, int d, int causal, long resident, int* sched,
   double best_us = -1.0;
   if ((long)B * H * N > 0 && resident > 0) {
     for (int s : cand) {
-      const dash::Geom G = dash::make_geom(s, causal, N, d);
+      const dash::Geom G = dash::make_geom(s, causal, N, d, (long)B * H);
       const long together = s == DASH_SCHED_SHIFT ? G.grp : s == DASH_SCHED_SYMSHIFT ? G.chains : 1;
       if (together > resident) continue;
       const double us = step_us(d, causal, s, N, (long)B * H);
@@ -429,9 +430,9 @@ int bwd_launch(const void* q, const void* k, const void* v, const void* o, const
   if (tickets == DASH_TICKETS_CHAIN_MAJOR && (sched == DASH_SCHED_SHIFT || sched == DASH_SCHED_SYMSHIFT))
     return fail(DASH_ERR_INVALID_ARG, "Shift and Symmetric Shift take the chains of a head together (head-major tickets)");
 
-  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  dash::Geom G = dash::make_geom(sched, causal, N, d, (long)B * H);
   bool xcd = false;
-  if ((rc = choose_placement(di, sched, causal, N, d, placement, &xcd)))
+  if ((rc = choose_placement(di, sched, causal, N, d, (long)B * H, placement, &xcd)))
     return rc;
   if (xcd) dash::place_on_xcds(G);
   const int nq = xcd ? di.nxcd : 1;  // ticket queues; workgroup i serves queue i % nq
@@ -633,7 +634,7 @@ int dash_bwd_placement(int B, int H, int N, int d, int causal, int schedule) {
   DeviceInfo di;
   if ((rc = device_info(&di))) return rc;
   bool xcd = false;
-  if ((rc = choose_placement(di, resolve(schedule, d, causal), causal, N, d, DASH_PLACEMENT_AUTO, &xcd)))
+  if ((rc = choose_placement(di, resolve(schedule, d, causal), causal, N, d, (long)B * H, DASH_PLACEMENT_AUTO, &xcd)))
     return rc;
   return xcd ? DASH_PLACEMENT_XCD : DASH_PLACEMENT_GLOBAL;
 }
@@ -683,15 +684,16 @@ void dash_release_workspace(void) {
   g_ws_bytes = 0;
 }
 
-int dash_schedule_table(int schedule, int N, int d, int causal, int placement, int* geometry, int* chain_len,
-                        int* task_kv, int* task_q, int* rank) {
-  int rc = check_shape(1, 1, N, d);
+int dash_schedule_table(int schedule, int heads, int N, int d, int causal, int placement, int* geometry,
+                        int* chain_len, int* task_kv, int* task_q, int* rank) {
+  if (heads < 1) return fail(DASH_ERR_INVALID_ARG, "heads must be >= 1");
+  int rc = check_shape(1, heads, N, d);
   if (rc) return rc;
   if ((rc = check_schedule(schedule, causal))) return rc;
   if (placement != DASH_PLACEMENT_GLOBAL && placement != DASH_PLACEMENT_XCD)
     return fail(DASH_ERR_INVALID_ARG, "placement must be DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD");
   const int sched = resolve(schedule, d, causal);
-  dash::Geom G = dash::make_geom(sched, causal, N, d);
+  dash::Geom G = dash::make_geom(sched, causal, N, d, heads);
   if (placement == DASH_PLACEMENT_XCD) dash::place_on_xcds(G);
   if (geometry) {
     geometry[0] = G.t_r;

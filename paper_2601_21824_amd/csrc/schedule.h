@@ -1,7 +1,7 @@
 // schedule.h -- closed-form dQ-reduction schedules, usable on host and device.
 //
-// One attention head of N rows is cut into KV tiles of BC rows (BC = 128 for
-// d <= 128, 64 for d = 256: one workgroup's resident K_j, V_j, dK_j, dV_j)
+// One attention head of N rows is cut into KV tiles of BC rows (kv_tile_rows:
+// one workgroup's resident K_j, V_j, dK_j, dV_j)
 // and scheduling Q tiles of br rows;
 // a scheduling Q tile is processed as br/64 physical 64-row blocks, each with
 // its own ordering counter.  A workgroup runs a "chain" of tasks (KV tile j,
@@ -46,7 +46,7 @@ namespace dash {
 enum Sched { S_ATOMIC = 0, S_NAIVE = 1, S_DESCENDING = 2, S_SHIFT = 3, S_SYMSHIFT = 4, S_PARTIALS = 6, S_SPLIT = 7 };
 
 constexpr int kBlockRows = 64;  // rows of a physical Q block (one counter each)
-constexpr int kTileKV = 128;    // KV rows per tile of the d = 64 / 128 kernel
+constexpr int kTileKV = 128;    // KV rows per tile of the d = 128 kernel
 constexpr int kMaxGroup = 256;  // Shift: KV-tile chains that must be co-resident
 constexpr int kXcdGroup = 32;   // ... under XCD-local placement (one XCD's resident workgroups)
 
@@ -64,14 +64,26 @@ struct Geom {
   int chain_major;  // work tickets chain-major (see ticket_chain), else head-major
 };
 
-// rows per KV tile for head dim d
-DASH_HD int kv_tile_rows(int d) { return d <= 128 ? 128 : 64; }
+// rows per KV tile: 128 at d = 128, 64 at d = 256.  At d = 64, 256 (the
+// 256-row kernel, half the accumulator traffic per FLOP) when the call has
+// KV tiles enough to keep a 256-CU GPU busy -- at least 256 of them over all
+// `heads` heads for a full mask, 1024 and N >= 2048 for a causal one (whose
+// chains are uneven) -- else 128.  The tile size is part of the summation
+// order, so it is a function of the problem (d, mask, N, heads) alone, never
+// of the device.
+DASH_HD int kv_tile_rows(int d, int causal, int N, long heads) {
+  if (d == 64) {
+    const long wide = heads * (long)((N + 255) / 256);
+    return (causal ? (N >= 2048 && wide >= 1024) : wide >= 256) ? 256 : 128;
+  }
+  return d == 128 ? 128 : 64;
+}
 
-DASH_HD Geom make_geom(int sched, int causal, int N, int d) {
+DASH_HD Geom make_geom(int sched, int causal, int N, int d, long heads) {
   Geom G;
   G.sched = sched;
   G.causal = causal ? 1 : 0;
-  G.bc = kv_tile_rows(d);
+  G.bc = kv_tile_rows(d, causal, N, heads);
   G.br = causal ? G.bc : kBlockRows;
   G.g = G.bc / G.br;
   G.t_c = (N + G.bc - 1) / G.bc;

@@ -11,6 +11,8 @@ the two is kept.  One JSON line per shape on stdout, in the format of
 ``bench.py --sweep``:
 
     python -m paper_2601_21824_amd.measure_model_grid > paper_2601_21824_amd/model_grid.jsonl
+
+(Head dims as arguments measure only those, e.g. ``... measure_model_grid 64``.)
 """
 from __future__ import annotations
 
@@ -21,8 +23,8 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def shapes():
-    for d in (64, 128, 256):
+def shapes(dims=(64, 128, 256)):
+    for d in dims:
         lengths = (4096, 8192, 16384, 32768) if d == 256 else (512, 1024, 2048, 4096, 8192, 16384)
         for causal in (False, True):
             for n in lengths:
@@ -32,7 +34,7 @@ def shapes():
                         yield d, causal, n, bh
 
 
-def main():
+def main(*dims):
     sys.path.insert(0, ROOT)
     import torch
 
@@ -41,7 +43,7 @@ def main():
     from paper_2601_21824_amd.synth import make_inputs
 
     ev = bench.HipEvents()
-    for d, causal, N, bh in shapes():
+    for d, causal, N, bh in shapes(tuple(int(x) for x in dims) or (64, 128, 256)):
         q, k, v, do = make_inputs(1, bh, N, d, seed=N + d + bh, sigma=0.5 if d == 256 else 1.0)
         qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
         og, lseg = dash.attn_fwd(qg, kg, vg, causal)
@@ -65,4 +67,4 @@ def main():
 
 
 if __name__ == "__main__":
-    sys.exit(main())
+    sys.exit(main(*sys.argv[1:]))

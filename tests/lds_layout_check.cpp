@@ -94,6 +94,39 @@ static void dst_patterns() {
   expect("d<=128 dS^T transposed reads (per wave and step)", rd, 0);
 }
 
+// d = 64 kernel with 256-row KV tiles (attn_bwd64w.hip): the Q / dO patterns
+// are tile_patterns<64>'s; new are the dS^T stores of 8 waves' worth of rows
+// (64 keys per wave), the K tile's transposed reads (A = K^T of dQ^T) and the
+// dS^T transposed reads over 256 keys
+static void w64_patterns() {
+  int wr = 0, rdk = 0, rdd = 0;
+  for (int w = 0; w < 4; ++w)
+    for (int kb = 0; kb < 2; ++kb)
+      for (int p = 0; p < 8; ++p) {
+        std::vector<long> a(64);
+        const int qb = p >> 2, half = (p >> 1) & 1, part = p & 1;
+        for (int l = 0; l < 64; ++l)
+          a[l] = 2L * dst_at(64 * w + 32 * kb + (l & 31), 32 * qb + 16 * half + 8 * part + 4 * (l >> 5));
+        wr += conflicts(a, 8);
+      }
+  for (int ks = 0; ks < 16; ++ks)
+    for (int blk = 0; blk < 2; ++blk)  // d block of the K^T operand / query half of dS^T
+      for (int dr = 0; dr < 8; dr += 4) {
+        std::vector<long> k(64), d(64);
+        for (int l = 0; l < 64; ++l) {
+          const int L16 = l & 15, nh = (l >> 4) & 1, g = l >> 5;
+          const int row = 16 * ks + 8 * g + (L16 >> 2) + dr, col = 32 * blk + 16 * nh + 4 * (L16 & 3);
+          k[l] = 2L * bf_at<64>(row, col);
+          d[l] = 2L * dst_at(row, col);
+        }
+        rdk += conflicts(k, 8);
+        rdd += conflicts(d, 8);
+      }
+  expect("d=64 256-row dS^T stores (all waves, per step)", wr, 0);
+  expect("d=64 256-row K^T transposed reads (per step, both d blocks)", rdk, 0);
+  expect("d=64 256-row dS^T transposed reads (per step, both halves)", rdd, 0);
+}
+
 static void d256_patterns() {
   int rows = 0, tr = 0, wr = 0, rd = 0;
   for (int qb = 0; qb < 4; ++qb)
@@ -158,6 +191,7 @@ int main() {
   tile_patterns<128>("d=128 Q/dO");
   tile_patterns<64>("d=64 Q/dO");
   dst_patterns();
+  w64_patterns();
   d256_patterns();
   std::printf(failures ? "FAIL\n" : "OK\n");
   return failures ? 1 : 0;

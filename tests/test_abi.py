@@ -74,7 +74,9 @@ def test_argument_errors_without_device():
     rc = lib.dash_attn_bwd_ex(*p, 1, 1, 128, 64, 0, 1, ctypes.c_float(0.125), ctypes.c_void_p(4096),
                               1 << 40, ctypes.byref(opts), None)
     assert rc == b.DASH_ERR_INVALID_ARG and "placement" in b.dash_last_error()
-    assert lib.dash_schedule_table(1, 128, 64, 0, 0, None, None, None, None, None) == b.DASH_ERR_INVALID_ARG
+    assert lib.dash_schedule_table(1, 1, 128, 64, 0, 0, None, None, None, None, None) == b.DASH_ERR_INVALID_ARG
+    assert lib.dash_schedule_table(1, 0, 128, 64, 0, b.DASH_PLACEMENT_GLOBAL, None, None, None, None, None) == \
+        b.DASH_ERR_INVALID_ARG
     # the MFMA peak measurement checks its arguments before touching the device
     assert lib.dash_mfma_peak(0, None) == b.DASH_ERR_INVALID_ARG
     out = ctypes.c_double(0.0)
@@ -102,17 +104,24 @@ KINDS = {b.DASH_SCHED_NAIVE: osched.NAIVE, b.DASH_SCHED_DESCENDING: osched.DESCE
 @pytest.mark.parametrize("N", [64, 200, 256, 1000, 1024, 4096, 4224, 8192, 16384, 32768])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("sched", [0, 1, 2, 3, 4, 6, 7])
-def test_schedule_table_matches_oracle(sched, causal, N, d, placement):
+@pytest.mark.parametrize("heads", [1, 64])
+def test_schedule_table_matches_oracle(heads, sched, causal, N, d, placement):
     if sched == b.DASH_SCHED_SYMSHIFT and not causal:
         pytest.skip("symshift is causal-only")
-    tab = b.dash_schedule_table(sched, N, d, causal, placement)
+    if heads > 1 and d != 64:
+        pytest.skip("the head count decides the tile size at d = 64 only")
+    tab = b.dash_schedule_table(sched, N, d, causal, placement, heads=heads)
     concrete = b.dash_resolve_schedule(sched, d, causal)
     kind = KINDS[concrete]
     t_r, t_c, br, bc, grp = tab["t_r"], tab["t_c"], tab["br"], tab["bc"], tab["group"]
-    # tile sizes: KV tiles of 128 rows (64 at d = 256); Q tiles of 64 rows (full)
-    # or KV-tile rows (causal); Shift groups of at most 256 chains, 32 when every
+    # tile sizes: KV tiles of 128 rows at d = 128, 64 at d = 256, and at d = 64
+    # 256 rows when the call has enough of them (full: 256 over all heads;
+    # causal: 1024 and N >= 2048), else 128; Q tiles of 64 rows (full) or
+    # KV-tile rows (causal); Shift groups of at most 256 chains, 32 when every
     # chain of a head runs on one XCD
-    assert bc == (128 if d <= 128 else 64)
+    wide = heads * -(-N // 256)
+    bc64 = 256 if ((N >= 2048 and wide >= 1024) if causal else wide >= 256) else 128
+    assert bc == {64: bc64, 128: 128, 256: 64}[d]
     assert br == (bc if causal else 64) and t_r * br == t_c * bc
     most = 32 if placement == b.DASH_PLACEMENT_XCD else 256
     assert grp == (min(t_c, most) if kind == osched.SHIFT else tab["chains"])

@@ -37,6 +37,11 @@ DET_CASES = [  # (B, H, N, d, causal, schedule[, placement])
     (2, 16, 8192, 128, False, "shift"),
     (2, 32, 8192, 128, True, "descending"),
     (2, 32, 8192, 128, True, "symshift"),
+    # d = 64 with 256-row KV tiles
+    (1, 128, 400, 64, False, "shift"),
+    (1, 128, 2100, 64, True, "descending"),
+    (1, 128, 2100, 64, True, "symshift"),
+    (2, 32, 8192, 64, False, "shift"),
 ]
 
 
@@ -128,6 +133,9 @@ PROTO_CASES = [
     (1, 2, 512, 256, False, "shift", GL),
     (1, 2, 512, 256, True, "symshift", GL),
     (1, 1, 333, 256, True, "descending", GL),
+    # d = 64 with 256-row KV tiles (enough of them over the call's heads)
+    (1, 128, 400, 64, False, "shift", GL),
+    (1, 128, 2048, 64, True, "symshift", GL),
     # every chain of a head on one XCD; at 33 KV tiles
     # Shift runs as two groups, 32 chains then 1
     (1, 2, 4224, 128, False, "shift", XL),
@@ -150,7 +158,7 @@ def test_witness_and_partial_sum_replay(case):
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=21)
     og, lseg = run_fwd(qg, kg, vg, causal)
     nblk = (N + 63) // 64
-    tab = dash.dash_schedule_table(sched, N, d, causal, placement)
+    tab = dash.dash_schedule_table(sched, N, d, causal, placement, heads=B * H)
     tc = (N + tab["bc"] - 1) // tab["bc"]  # KV tiles (before Symmetric Shift's padding)
     witness = torch.full((B * H, nblk, tc), -1, dtype=torch.int32, device="cuda")
     partials = torch.full((B * H, tc, N, d), float("nan"), dtype=torch.float32, device="cuda")
@@ -200,7 +208,7 @@ def test_grid_size_does_not_change_bits(case):
     og, lseg = run_fwd(qg, kg, vg, causal)
     ws = dash.new_workspace(B, H, N, d)
     for place, queues in ((GL, 1), (XL, 8)):  # MI355X: 8 XCDs, one queue each
-        tab = dash.dash_schedule_table(sched, N, d, causal, place)
+        tab = dash.dash_schedule_table(sched, N, d, causal, place, heads=B * H)
         together = (tab["group"] if sched in ("shift", "symshift") else 1) * queues
         opts = lambda cap: dash.dash_bwd_options_t(0, 0, None, None, None, None, None, cap, 0, place)
         ref = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=ws, options=opts(0))
@@ -290,8 +298,8 @@ def test_placement(case):
     assert dash.dash_bwd_check(ws) == dash.DASH_OK
     for a_, b_ in zip(auto, glob):
         assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
-    tab_x = dash.dash_schedule_table(sched, N, d, causal, XL)
-    tab_g = dash.dash_schedule_table(sched, N, d, causal, GL)
+    tab_x = dash.dash_schedule_table(sched, N, d, causal, XL, heads=B * H)
+    tab_g = dash.dash_schedule_table(sched, N, d, causal, GL, heads=B * H)
     if np.array_equal(tab_x["rank"], tab_g["rank"]):
         for a_, b_ in zip(xcd, glob):
             assert torch.equal(a_.view(torch.int16), b_.view(torch.int16))
@@ -365,7 +373,7 @@ def test_shift_groups_order_and_minimal_grid(d):
     print(f"\n[groups] N={N} d={d}", flush=True)
     _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=41, sigma=0.5)
     og, lseg = run_fwd(qg, kg, vg, causal)
-    tab = dash.dash_schedule_table("shift", N, d, causal)
+    tab = dash.dash_schedule_table("shift", N, d, causal, heads=B * H)
     assert tab["t_c"] == 512 and tab["group"] == 256
     nblk = (N + 63) // 64
     witness = torch.full((B * H, nblk, tab["t_c"]), -1, dtype=torch.int32, device="cuda")

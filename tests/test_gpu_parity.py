@@ -34,6 +34,9 @@ CASES = [
     (2, 1, 333, 256, False),
     (2, 1, 333, 256, True),
     (1, 1, 1, 256, True),
+    # 128 heads of 400 rows at d = 64: enough KV tiles for 256-row tiles
+    # (attn_bwd64w.hip), ragged last tile
+    (1, 128, 400, 64, False),
 ]
 
 _cache = {}
@@ -97,10 +100,17 @@ FULL_HEADS = [
     (2, 32, 8192, 128, True, "descending"),
     (2, 32, 8192, 128, True, "symshift"),
     (2, 32, 8192, 128, True, "atomic"),
+    # d = 64 with 256-row KV tiles: the 16384-token full sweep's N = 8192
+    # point (64 heads) and a causal call of 128 heads past N = 2048
+    (2, 32, 8192, 64, False, "shift"),
+    (2, 32, 8192, 64, False, "naive"),
+    (1, 128, 2100, 64, True, "descending"),
+    (1, 128, 2100, 64, True, "symshift"),
+    (1, 128, 2100, 64, True, "atomic"),
 ]
 
 
-@pytest.mark.parametrize("case", FULL_HEADS, ids=[f"B{c[0]}H{c[1]}N{c[2]}{'c' if c[4] else 'f'}-{c[5]}" for c in FULL_HEADS])
+@pytest.mark.parametrize("case", FULL_HEADS, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}-{c[5]}" for c in FULL_HEADS])
 def test_full_size_whole_heads(case):
     """Full-size workloads: every dQ, dK, dV (and O) entry of the first and
     last head against the oracle; over every head, sum_j dV_j = sum_i dO_i

@@ -37,7 +37,7 @@ def test_wait_stats(case):
     for a, b in zip(plain, inst):
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     late, wait_ticks, wave_ticks = (int(x) for x in stats.cpu())
-    tab = dash.dash_schedule_table(sched, N, d, causal, place or dash.DASH_PLACEMENT_GLOBAL)
+    tab = dash.dash_schedule_table(sched, N, d, causal, place or dash.DASH_PLACEMENT_GLOBAL, heads=B * H)
     sub = tab["br"] // 64  # kernel steps (64-row blocks) per scheduled Q tile
     wave_steps = 4 * B * H * int(tab["chain_len"].sum()) * sub
     # a block's first contributor (rank 0) always sees its turn early: every

@@ -70,14 +70,18 @@ def test_model_equals_oracle_simulator(kind, causal, n, heads, workers, chain_ma
 
 def test_model_ragged_length():
     """Steps past N are left out, as the kernels skip them.  A full-mask head of
-    130 rows at d = 64 has KV tiles 0 and 1 and blocks 0..2 (block 3 starts
+    130 rows at d = 128 has KV tiles 0 and 1 and blocks 0..2 (block 3 starts
     past N); naive runs both chains over blocks 0, 1, 2, and tile 1 reduces each
     block right after tile 0: one step behind, 4 steps in all."""
-    one = b.dash_model_makespan("naive", 1, 1, 130, 64, False, 64, 0.0, 1.0, ticket_order=b.DASH_TICKETS_HEAD_MAJOR)
+    one = b.dash_model_makespan("naive", 1, 1, 130, 128, False, 64, 0.0, 1.0, ticket_order=b.DASH_TICKETS_HEAD_MAJOR)
     assert one == pytest.approx(4.0)
     # the same head at 192 rows still has 3 blocks; at 193 a fourth appears
-    assert b.dash_model_makespan("naive", 1, 1, 192, 64, False, 64, 0.0, 1.0) == pytest.approx(4.0)
-    assert b.dash_model_makespan("naive", 1, 1, 193, 64, False, 64, 0.0, 1.0) == pytest.approx(5.0)
+    assert b.dash_model_makespan("naive", 1, 1, 192, 128, False, 64, 0.0, 1.0) == pytest.approx(4.0)
+    assert b.dash_model_makespan("naive", 1, 1, 193, 128, False, 64, 0.0, 1.0) == pytest.approx(5.0)
+    # at d = 64 one head keeps 128-row tiles (4 steps); a call of 256 heads
+    # takes 256-row tiles, one chain of 3 steps per head, all at once
+    assert b.dash_model_makespan("naive", 1, 1, 130, 64, False, 64, 0.0, 1.0) == pytest.approx(4.0)
+    assert b.dash_model_makespan("naive", 1, 256, 130, 64, False, 256, 0.0, 1.0) == pytest.approx(3.0)
 
 
 def test_model_head_cap_scales():
