@@ -248,6 +248,8 @@ def main():
     main_tflops = flops / (main_ms * 1e-3) / 1e12
     placement = "global" if det == "atomic" else \
         ("XCD-local" if dash.dash_bwd_placement(B, H, N, d, causal, det) == dash.DASH_PLACEMENT_XCD else "global")
+    bc = dash.dash_schedule_table(det, N, d, causal, heads=B * H)["bc"]
+    kname = "bwd_main256_kernel" if d == 256 else ("bwd_main64w_kernel" if bc == 256 else "bwd_main_kernel")
     out = {
         "metric": "deterministic attn-bwd TFLOPS (bf16, d=128, N=8192) + % of atomic variant",
         "value": round(tflops, 2),
@@ -268,7 +270,7 @@ def main():
         "pct_of_atomic": round(100.0 * tflops / results["atomic"][2], 2),
         "atomic_tflops": round(results["atomic"][2], 2),
         "naive_tflops": round(results["naive"][2], 2) if "naive" in results else None,
-        "roofline": {"bound": "mfma", "kernel": f"bwd_main{'256' if d == 256 else ''}_kernel<{d}, "
+        "roofline": {"bound": "mfma", "kernel": f"{kname}<{d}, "
                                f"{'causal' if causal else 'full'} mask, {'atomic' if det == 'atomic' else 'ordered'}>"
                                f", placement {placement}",
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
