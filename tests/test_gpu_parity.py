@@ -211,9 +211,11 @@ def test_long_d256_sampled(causal, sched):
     assert zero < 1e-2 and rel < 5e-3, (float(zero), float(rel))
 
 
-@pytest.mark.parametrize("d", [64, 128, 256])
-@pytest.mark.parametrize("causal", [False, True])
-def test_ragged_tail_next_head_with_very_negative_lse(d, causal):
+RAGGED = [(d, c, 2) for d in (64, 128, 256) for c in (False, True)] + [(64, False, 256)]
+
+
+@pytest.mark.parametrize("d,causal,H", RAGGED, ids=[f"d{d}{'c' if c else 'f'}H{h}" for d, c, h in RAGGED])
+def test_ragged_tail_next_head_with_very_negative_lse(d, causal, H):
     """N = 200 leaves padded query rows in each head's last 64-row block and
     padded keys in its last KV tile.  Query 0 of head 1 is built with a
     logsumexp far below -88 (natural log): with a causal mask it sees only key
@@ -225,8 +227,9 @@ def test_ragged_tail_next_head_with_very_negative_lse(d, causal):
     into NaN: the padded rows of head 0 must read L = D = 0 within their own
     head's bounds, not head 1's first row; and the padded keys of head 1
     (S = 0, their K rows read as zero) must not give P = exp(-L) in row 0.
-    Every schedule against the oracle."""
-    B, H, N = 1, 2, 200
+    Every schedule against the oracle; with 256 heads at d = 64 the call
+    takes 256-row KV tiles."""
+    B, N = 1, 200
     q, k, v, do = make_inputs(B, H, N, d, seed=404)
     q, k, do = q.clone(), k.clone(), do.clone()
     q[0, 1, 0] = 0.0
