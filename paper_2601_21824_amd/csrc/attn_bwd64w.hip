@@ -240,6 +240,7 @@ __global__ __launch_bounds__(256) void bwd_main64w_kernel(BwdArgs a) {
       // LDS reads below are per-lane byte offsets computed once per run from
       // a fresh lane index, plus compile-time offsets: each swizzle depends
       // only on row bits that the compile-time part leaves alone
+      const int slf = fresh_lane() & 63;  // this step's lane index, for every LDS address below
       auto at16 = [](const void* base, uint32_t off) { return *(const bf16x8*)((const char*)base + off); };
       auto tr_at = [](const void* base, uint32_t off) { return tr_read((const __bf16*)((const char*)base + off)); };
 
@@ -255,7 +256,7 @@ __global__ __launch_bounds__(256) void bwd_main64w_kernel(BwdArgs a) {
       f32x16 s[2], dp[2];
       auto sdp = [&](int qb, int kb, auto&& extra) {
         bf16x8 rq[KS], ro[KS];
-        const int lf = fresh_lane() & 63;
+        const int lf = slf;
         // row 32qb + lc: rows 32 apart share the swizzle
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -321,7 +322,7 @@ __global__ __launch_bounds__(256) void bwd_main64w_kernel(BwdArgs a) {
       auto store_ds_piece = [&](int kb, int k) {
         const int qb = k >> 2, half = (k >> 1) & 1, part = k & 1;
         const u32x4 dv4 = __builtin_bit_cast(u32x4, dsbf[qb][half]);
-        const int lf = fresh_lane() & 63;
+        const int lf = slf;
         // rows 64w + 32kb + lc share lc's swizzle
         *(u32x2*)((char*)sm.dst + dst_at(lf & 31, 32 * qb + 16 * half + 8 * part + 4 * (lf >> 5)) * 2 +
                   (64 * w + 32 * kb) * BM * 2) =
@@ -332,7 +333,7 @@ __global__ __launch_bounds__(256) void bwd_main64w_kernel(BwdArgs a) {
       // iteration k = (d block, 16-query half)
       auto dvdk = [&](int qb, int kb, auto&& extra) {
         constexpr int NP = 2 * NB;
-        const int lf = fresh_lane() & 63;
+        const int lf = slf;
         // rows 32qb + 16half + x and x + 8 (x < 8): the swizzle of x and x + 8
         auto rd = [&](int k, bf16x8* bo, bf16x8* bq) {
           const int nb = k >> 1, half = k & 1;
@@ -430,7 +431,7 @@ __global__ __launch_bounds__(256) void bwd_main64w_kernel(BwdArgs a) {
         for (int r = 0; r < 16; ++r) dq[r] = 0.f;
         {
           constexpr int RING = 4;
-          const int lf = fresh_lane() & 63;
+          const int lf = slf;
           // keys 16ks + x and x + 4 (x < 12): the K tile's swizzle repeats
           // every 16 rows, dS^T's every 32 (two bases, even and odd ks)
           auto rd = [&](int ks, bf16x8* ka, bf16x8* db) {
