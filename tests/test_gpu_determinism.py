@@ -272,6 +272,10 @@ PLACE_CASES = [
     (1, 8, 4096, 256, False, "shift"),
     (1, 8, 2048, 256, True, "descending"),
     (2, 4, 2048, 256, True, "symshift"),
+    # d = 64 with 256-row KV tiles (64 heads x 8 tiles)
+    (2, 32, 2048, 64, False, "shift"),
+    (2, 32, 2048, 64, False, "naive"),
+    (1, 128, 2048, 64, True, "descending"),
 ]
 
 

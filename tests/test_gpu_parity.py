@@ -37,6 +37,7 @@ CASES = [
     # 128 heads of 400 rows at d = 64: enough KV tiles for 256-row tiles
     # (attn_bwd64w.hip), ragged last tile
     (1, 128, 400, 64, False),
+    (1, 256, 33, 64, False),
 ]
 
 _cache = {}
