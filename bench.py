@@ -10,7 +10,10 @@ B=2, H=16, N=8192, d=128, full mask (16384 tokens, hidden 2048), inputs bf16
   pct_of_atomic that throughput as a percentage of the atomic-add variant's
   roofline     the main kernel's algorithmic MFMA FLOPs per launch divided by
                its mean duration (HIP events recorded by the library on the
-               launch stream around that kernel), against the bf16 dense peak
+               launch stream around that kernel), against the bf16 dense peak;
+               with the per-call median and minimum of that duration
+  spinup       the untimed calls run first so that the device is at its
+               steady clock before the first schedule's warm-up
   cpu_baseline the fp64 oracle timed on the host on one full head of the
                same workload, scaled to the same FLOP count
 """
@@ -20,6 +23,7 @@ import argparse
 import ctypes
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -53,7 +57,10 @@ class HipEvents:
         self.hip.hipEventDestroy(e)
 
 
-def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
+def time_schedule(dash, tensors, causal, sched, steps, warmup, ev, samples=None):
+    """Mean wall-clock ms per call over `steps` back-to-back calls, and the mean
+    main-kernel ms from HIP events around each call's main kernel (appended
+    per call to `samples` when given)."""
     import torch
     q, k, v, o, do, lse, dq, dk, dv, ws = tensors
     for _ in range(warmup):  # each warm-up call is checked (the check synchronizes)
@@ -71,6 +78,8 @@ def time_schedule(dash, tensors, causal, sched, steps, warmup, ev):
     if dash.dash_bwd_check(ws) != dash.DASH_OK:
         raise RuntimeError(f"{sched}: ordering wait timed out")
     main_ms = [ev.elapsed_ms(a, b) for a, b in pairs]
+    if samples is not None:
+        samples.extend(main_ms)
     for a, b in pairs:
         ev.destroy(a)
         ev.destroy(b)
@@ -254,9 +263,11 @@ def main():
     ev = HipEvents()
 
     results = {}
+    per_call = {}
     spin_calls = spin_up(dash, tensors, causal, scheds[0], args.spinup_ms)
     for sched in dict.fromkeys(scheds):
-        ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev)
+        per_call[sched] = []
+        ms, main_ms = time_schedule(dash, tensors, causal, sched, args.steps, args.warmup, ev, per_call[sched])
         results[sched] = (ms, main_ms, flops / (ms * 1e-3) / 1e12)
         print(f"[bench] {sched}: {ms:.3f} ms/step, main kernel {main_ms:.3f} ms, "
               f"{results[sched][2]:.1f} TFLOPS", file=sys.stderr, flush=True)
@@ -298,7 +309,9 @@ def main():
                      "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic() if (N, d, causal, det) == (8192, 128, False, "shift") else None,
-                     "main_kernel_ms": round(main_ms, 4)},
+                     "main_kernel_ms": round(main_ms, 4),
+                     "main_kernel_ms_median": round(statistics.median(per_call[det]), 4),
+                     "main_kernel_ms_min": round(min(per_call[det]), 4)},
     }
     # the measured MFMA peak of this device beside the published one
     measured = dash.dash_mfma_peak()
