@@ -3,7 +3,8 @@ it) against the fp64 oracle, element by element, at sizes that span several
 tiles, ragged tails and both masks; plus sampled outputs at the full sizes of
 the workloads: the 16384-token sweeps at N = 8192 (16 heads of 128, full
 mask; 32 heads of 128, causal) and N = 16384, and the long-sequence
-head-dim-256 workload (B=1, H=8, N=32768, d=256, both masks)."""
+head-dim-256 workload (B=1, H=8, N=32768, d=256, both masks); and seeded
+shapes off that grid, half of them at an explicit softmax scale."""
 import numpy as np
 import pytest
 import torch
@@ -253,3 +254,67 @@ def test_ragged_tail_next_head_with_very_negative_lse(d, causal, H):
         for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
             rf, rm = assert_close(f"{sched} {name}", got, ref)
             print(f"  {sched} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
+
+
+def _random_cases(n=20, seed=2601):
+    """Seeded shapes off the hand-picked grid: every head dim and mask, N
+    uniform or log-uniform in 1 .. 700 (ragged in both tile sizes), 1-10 heads, an
+    explicit softmax scale in half of them (0.5 - 1.5 / sqrt(d)), input scale
+    0.5 or 1; every fifth case is a d = 64 call of 100-160 heads of 257-420
+    rows, alternately full (256-row KV tiles once the heads give 256 or more
+    of them) and causal."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = int(rng.choice([64, 128, 256]))
+        causal = bool(rng.integers(2))
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 6))
+        N = int(rng.integers(1, 701)) if rng.integers(2) else max(1, int(np.exp(rng.uniform(0.0, np.log(700.0)))))
+        if i % 5 == 4:
+            d, B, H, N = 64, 1, int(rng.integers(100, 161)), int(rng.integers(257, 421))
+            causal = i % 10 == 9
+        scale = float(rng.uniform(0.5, 1.5) / np.sqrt(d)) if rng.integers(2) else None
+        sigma = float(rng.choice([0.5, 1.0]))
+        out.append((B, H, N, d, causal, scale, sigma, int(rng.integers(1 << 30))))
+    return out
+
+
+RANDOM = _random_cases()
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[f"B{c[0]}H{c[1]}N{c[2]}d{c[3]}{'c' if c[4] else 'f'}"
+                                              f"{'' if c[5] is None else '-s%.3f' % c[5]}" for c in RANDOM])
+def test_random_shapes_match_oracle(case):
+    """Forward and every backward schedule (and AUTO) against the oracle at the
+    same softmax scale, element by element."""
+    B, H, N, d, causal, scale, sigma, seed = case
+    print(f"\n[random] B={B} H={H} N={N} d={d} causal={causal} scale={scale} sigma={sigma} seed={seed}", flush=True)
+    q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, seed, sigma)
+    ref_o, ref_l = oracle.attn_fwd(q, k, v, causal, scale=scale)
+    rdq, rdk, rdv, _, _ = oracle.attn_bwd(q, k, v, do, causal, scale=scale)
+    og, lseg = dash_fwd(qg, kg, vg, causal, scale)
+    assert_close("O", og, ref_o)
+    np.testing.assert_allclose(lseg.cpu().double().numpy(), ref_l, rtol=2e-5, atol=2e-5)
+    for sched in schedules(causal, d) + ("auto",):
+        dq, dk, dv = dash_bwd(qg, kg, vg, og, dog, lseg, causal, sched, scale)
+        for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
+            rf, rm = assert_close(f"{sched} {name}", got, ref)
+            print(f"  {sched} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
+
+
+def dash_fwd(qg, kg, vg, causal, scale):
+    from paper_2601_21824_amd import binding as dash
+    o, lse = dash.attn_fwd(qg, kg, vg, causal, scale=scale)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def dash_bwd(qg, kg, vg, og, dog, lseg, causal, sched, scale):
+    from paper_2601_21824_amd import binding as dash
+    # an explicit scale goes through the workspace form of the call
+    ws = None if scale is None else dash.new_workspace(*qg.shape, "partials" if sched == "partials" else "shift")
+    dq, dk, dv = dash.attn_bwd(qg, kg, vg, og, dog, lseg, causal, sched, scale=scale, workspace=ws)
+    torch.cuda.synchronize()
+    if ws is not None:
+        assert dash.dash_bwd_check(ws) == dash.DASH_OK, f"{sched}: ordering wait timed out"
+    return dq, dk, dv
