@@ -261,7 +261,8 @@ int dash_resolve_schedule(int schedule, int d, int causal);
    nothing was calibrated for this d and mask, or the problem is empty).  The
    first call for a shape simulates (at most enough heads to fill the
    workgroups three times; milliseconds of host time), later ones read a
-   per-process cache. */
+   per-process cache of up to 4096 shapes (a full cache starts over; the
+   choice is a pure function of the shape and the workgroup count). */
 int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int* schedule, double* predicted_ms);
 
 /* Section 3.1's DAG model of a backward call with explicit costs: every block

@@ -312,8 +312,12 @@ long model_head_cap(long chains, long resident) {
 // calibrated model predicts for this shape (ties: the mask's default, Shift /
 // Descending).  Candidates the device cannot run (a Shift group or a head's
 // Symmetric Shift chains beyond the resident workgroups) are left out.  A
-// shape is simulated once per process; at most enough heads to fill the
-// workgroups three times are simulated.
+// shape is simulated once per process while the cache holds it (up to
+// kAutoCacheShapes shapes; then it starts over, which only costs the
+// simulations again: the pick is a pure function of the shape and the
+// device); at most enough heads to fill the workgroups three times are
+// simulated.
+constexpr size_t kAutoCacheShapes = 4096;
 std::mutex g_auto_mu;
 std::map<std::tuple<int, int, int, int, int, long>, std::pair<int, double>> g_auto;
 
@@ -349,6 +353,7 @@ int auto_pick(int B, int H, int N, int d, int causal, long resident, int* sched,
   }
   const double best_ms = best_us < 0 ? -1.0 : best_us * 1e-3;
   std::lock_guard<std::mutex> lk(g_auto_mu);
+  if (g_auto.size() >= kAutoCacheShapes) g_auto.clear();
   g_auto[key] = {best, best_ms};
   *sched = best;
   if (ms) *ms = best_ms;

@@ -140,3 +140,13 @@ def test_model_argument_checks():
         b.dash_model_makespan("symshift", 1, 1, 512, 128, False, 16, 1.0, 1.0)
     with pytest.raises(b.DashError):
         b.dash_auto_schedule(1, 1, 512, 96, False, 256)
+
+
+def test_auto_cache_starts_over_with_the_same_answers():
+    """The per-process cache of AUTO picks holds up to 4096 shapes; past that
+    it is cleared, and a shape simulated again gets the same pick."""
+    shapes = [(2, 16, 8192, 128, False), (2, 32, 8192, 128, True), (1, 8, 4096, 256, False)]
+    first = [b.dash_auto_schedule(*s, 256) for s in shapes]
+    for n in range(1, 4200):
+        b.dash_auto_schedule(1, 1, n, 64, n % 2 == 1, 256)
+    assert [b.dash_auto_schedule(*s, 256) for s in shapes] == first
