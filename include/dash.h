@@ -272,8 +272,9 @@ int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int*
    DESCENDING, SHIFT or SYMSHIFT (SHIFT with causal != 0 is SYMSHIFT);
    ticket_order as in dash_bwd_options_t (AUTO: the library's order for
    `workers` resident workgroups).  max_heads = 0 simulates all B*H heads
-   (host time grows with B*H*N^2); max_heads > 0 simulates at most that many
-   and scales the makespan by B*H / max_heads (dash_auto_schedule uses
+   (host time grows with B*H*N^2); with max_heads > 0 and B*H > 2 * max_heads
+   it simulates max_heads and 2 * max_heads heads and extrapolates linearly
+   in the number of heads (dash_auto_schedule uses max_heads =
    ceil(3 * workers / chains per head)).  *makespan receives the critical
    path in the units of c and r.  DASH_ERR_UNSUPPORTED when chains that must
    run together exceed `workers` (no chain can finish); no device needed. */

@@ -7,8 +7,8 @@ script as model_grid.jsonl.  For every ordered schedule of every line,
 the call's measured time is divided by the makespan the model gives that
 shape with a unit block step (compute share kModelComputeShare, the rest
 reduction), simulated exactly as the library does for DASH_SCHED_AUTO (256
-resident workgroups, the library's ticket order, ceil(3 * 256 / chains)
-heads).  At a sweep shape the model then reproduces the measured time of
+resident workgroups, the library's ticket order, and for many heads the
+extrapolation from ceil(3 * 256 / chains) and twice that many heads).  At a sweep shape the model then reproduces the measured time of
 every schedule, and AUTO picks the measured fastest; elsewhere the step time
 is interpolated in N and in the number of heads, and the DAG decides.
 

@@ -288,8 +288,16 @@ double step_us(int d, int causal, int sched, int N, long heads) {
 }
 
 // Makespan of B*H heads on `workers` workgroups with compute c and reduction
-// r per block step; `head_cap` > 0 simulates at most that many heads and
-// scales the result to B*H.  Returns < 0 if the model deadlocks.
+// r per block step.  With `head_cap` > 0 and more than 2 * head_cap heads,
+// head_cap and 2 * head_cap heads are simulated and the makespan is
+// extrapolated linearly in the number of heads: once the workgroups are
+// full, every further head adds the same time, while the pipeline fill and
+// the last partial round are paid once (scaling one simulation by
+// B*H / head_cap would charge those once per head_cap heads).  Where the
+// fill shrinks as heads are added (chain-major tickets spread it over more
+// heads), the line can fall below what the steps alone need: the result is
+// kept at or above that bound, every workgroup busy from start to end (and
+// no less than the longest chain).  Returns < 0 if the model deadlocks.
 double model_makespan(int sched, int B, int H, int N, int d, int causal, long workers, int tickets, double c,
                       double r, long head_cap) {
   dash::Geom G = dash::make_geom(sched, causal, N, d, (long)B * H);
@@ -297,12 +305,20 @@ double model_makespan(int sched, int B, int H, int N, int d, int causal, long wo
                                                : auto_chain_major(sched, causal, d, G.chains, workers, false);
   const dash::HeadDag hd = dash::build_head_dag(G, N);
   const long heads = (long)B * H;
-  const long sim = head_cap > 0 && heads > head_cap ? head_cap : heads;
-  const double m = dash::simulate_dag(G, hd, (int)sim, (int)workers, c, r);
-  return m < 0 ? m : m * (double)heads / (double)sim;
+  if (head_cap <= 0 || heads <= 2 * head_cap) return dash::simulate_dag(G, hd, (int)heads, (int)workers, c, r);
+  const double m1 = dash::simulate_dag(G, hd, (int)head_cap, (int)workers, c, r);
+  const double m2 = dash::simulate_dag(G, hd, (int)(2 * head_cap), (int)workers, c, r);
+  if (m1 < 0 || m2 < 0) return -1.0;
+  const double line = m2 + (m2 - m1) * (double)(heads - 2 * head_cap) / (double)head_cap;
+  int longest = 0;
+  for (int w = 0; w < G.chains; ++w) longest = std::max(longest, hd.off[w + 1] - hd.off[w]);
+  const double bound = std::max((double)hd.off[G.chains] * (double)heads * (c + r) / (double)workers,
+                                (double)longest * (c + r));
+  return std::max(line, bound);
 }
 
-// Heads simulated for DASH_SCHED_AUTO: enough to fill the workgroups three times.
+// Head cap of DASH_SCHED_AUTO's simulations: enough heads to fill the
+// workgroups three times (and twice that for the extrapolation).
 long model_head_cap(long chains, long resident) {
   const long cap = (3 * resident + chains - 1) / chains;
   return cap > 0 ? cap : 1;
@@ -315,8 +331,8 @@ long model_head_cap(long chains, long resident) {
 // shape is simulated once per process while the cache holds it (up to
 // kAutoCacheShapes shapes; then it starts over, which only costs the
 // simulations again: the pick is a pure function of the shape and the
-// device); at most enough heads to fill the workgroups three times are
-// simulated.
+// device); a call with many heads is simulated at enough heads to fill the
+// workgroups three and six times and extrapolated (model_makespan).
 constexpr size_t kAutoCacheShapes = 4096;
 std::mutex g_auto_mu;
 std::map<std::tuple<int, int, int, int, int, long>, std::pair<int, double>> g_auto;

@@ -2,8 +2,8 @@
 behind the block-step times of the DAG model that picks DASH_SCHED_AUTO.
 
 For d in (64, 128, 256), both masks, N from 512 to 16384 (d = 256: 4096 to
-32768) and B*H from 1 to 256 heads (at most 2^21 tokens and 6e13 FLOPs per
-call), every
+32768) and B*H of 1, 4, 16, 32, 64, 128 and 256 heads (at most 2^21 tokens
+and 6e13 FLOPs per call), every
 candidate deterministic schedule is timed as bench.py times a backward call
 (whole call, wall clock over back-to-back calls after 3 checked warm-up
 calls, >= 20 ms of work per timing), twice in opposite orders; the better of
@@ -12,7 +12,8 @@ the two is kept.  One JSON line per shape on stdout, in the format of
 
     python -m paper_2601_21824_amd.measure_model_grid > paper_2601_21824_amd/model_grid.jsonl
 
-(Head dims as arguments measure only those, e.g. ``... measure_model_grid 64``.)
+(Head dims as arguments measure only those, e.g. ``... measure_model_grid 64``;
+``--heads 32,128`` only those head counts.)
 """
 from __future__ import annotations
 
@@ -23,12 +24,15 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def shapes(dims=(64, 128, 256)):
+HEADS = (1, 4, 16, 32, 64, 128, 256)
+
+
+def shapes(dims=(64, 128, 256), heads=HEADS):
     for d in dims:
         lengths = (4096, 8192, 16384, 32768) if d == 256 else (512, 1024, 2048, 4096, 8192, 16384)
         for causal in (False, True):
             for n in lengths:
-                for bh in (1, 4, 16, 64, 256):
+                for bh in heads:
                     flops = 4.0 * bh * n * n * d * 2.5 / (2 if causal else 1)
                     if bh * n <= (1 << 21) and flops <= 6e13:
                         yield d, causal, n, bh
@@ -42,8 +46,13 @@ def main(*dims):
     from paper_2601_21824_amd import binding as dash
     from paper_2601_21824_amd.synth import make_inputs
 
+    heads = HEADS
+    if "--heads" in dims:
+        i = dims.index("--heads")
+        heads = tuple(int(x) for x in dims[i + 1].split(","))
+        dims = dims[:i] + dims[i + 2:]
     ev = bench.HipEvents()
-    for d, causal, N, bh in shapes(tuple(int(x) for x in dims) or (64, 128, 256)):
+    for d, causal, N, bh in shapes(tuple(int(x) for x in dims) or (64, 128, 256), heads):
         q, k, v, do = make_inputs(1, bh, N, d, seed=N + d + bh, sigma=0.5 if d == 256 else 1.0)
         qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
         og, lseg = dash.attn_fwd(qg, kg, vg, causal)

@@ -84,6 +84,30 @@ def test_model_ragged_length():
     assert b.dash_model_makespan("naive", 1, 256, 130, 64, False, 256, 0.0, 1.0) == pytest.approx(3.0)
 
 
+EXTRAP = [(s, c, d, n, h) for s, c in (("shift", False), ("naive", False), ("descending", False), ("naive", True),
+                                       ("descending", True), ("symshift", True))
+          for d, n, h in ((64, 6144, 128), (64, 12288, 128), (128, 2048, 512), (128, 3072, 200), (256, 8192, 40))]
+
+
+@pytest.mark.parametrize("sched,causal,d,n,heads", EXTRAP)
+def test_model_extrapolation_in_heads(sched, causal, d, n, heads):
+    """With max_heads the model simulates max_heads and twice that many heads
+    and extrapolates linearly in the number of heads, held at or above the
+    steps' own bound.  Against the simulation of every head, at the cap AUTO
+    uses (three rounds of 256 workgroups): within 5%, and exact for Shift
+    where a head's chains do not divide the workgroups
+    (48 or 24 chains per head), the case that scaling one simulation by
+    heads / max_heads overcharged by 25-30%."""
+    chains = b.dash_schedule_table(sched, n, d, causal, heads=heads)["chains"]
+    cap = -(-3 * 256 // chains)
+    full = b.dash_model_makespan(sched, 1, heads, n, d, causal, 256, 0.02, 0.98)
+    ext = b.dash_model_makespan(sched, 1, heads, n, d, causal, 256, 0.02, 0.98, max_heads=cap)
+    # up to twice the cap every head is simulated
+    assert ext == pytest.approx(full, rel=5e-2 if heads > 2 * cap else 1e-12)
+    if sched == "shift" and n in (6144, 12288):
+        assert ext == pytest.approx(full, rel=1e-12)
+
+
 def test_model_head_cap_scales():
     full = b.dash_model_makespan("shift", 1, 8, 1024, 128, False, 16, 0.1, 0.9)
     capped = b.dash_model_makespan("shift", 1, 8, 1024, 128, False, 16, 0.1, 0.9, max_heads=2)
