@@ -259,8 +259,9 @@ int dash_resolve_schedule(int schedule, int d, int causal);
    device's, which needs the device).  *schedule receives the choice and
    *predicted_ms (if not NULL) the predicted makespan in milliseconds (-1 when
    nothing was calibrated for this d and mask, or the problem is empty).  The
-   first call for a shape simulates (at most enough heads to fill the
-   workgroups three times; milliseconds of host time), later ones read a
+   first call for a shape simulates (enough heads to fill the workgroups three
+   and six times, extrapolated, when the call has more; 0.1-1 s of host time
+   at large N), later ones read a
    per-process cache of up to 4096 shapes (a full cache starts over; the
    choice is a pure function of the shape and the workgroup count). */
 int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int* schedule, double* predicted_ms);
