@@ -1,0 +1,15 @@
+"""bench.py's command line without a GPU: a run on more than one GPU is
+refused with a message and exit status 2 before anything touches a device."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert p.returncode == 2
+    assert "one GPU" in p.stderr or "single MI355X" in p.stderr
+    assert p.stdout == ""
