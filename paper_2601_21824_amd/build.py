@@ -24,9 +24,11 @@ HIPCC_FLAGS = [
     "-Wno-unused-command-line-argument",
 ]
 # per-source flags: the 256-row d = 64 kernel runs faster with its MFMA
-# results in VGPRs (S and dP feed the softmax without AGPR reads); the d = 128
-# kernel, with less room in its VGPRs, does not
-SOURCE_FLAGS = {"attn_bwd64w.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# results in VGPRs (S and dP feed the softmax without AGPR reads), and the
+# d = 256 kernel compiles that way without the VGPR spills (and scratch) it
+# has otherwise; the d = 128 kernel, with less room in its VGPRs, runs slower
+_VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+SOURCE_FLAGS = {"attn_bwd64w.hip": _VGPR_MFMA, "attn_bwd256.hip": _VGPR_MFMA}
 
 
 def hipcc() -> str:
