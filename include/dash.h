@@ -183,9 +183,10 @@ int dash_attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float
  * fixed by `schedule`, serialized by per-Q-block counters (no atomics on the
  * data), except for DASH_SCHED_ATOMIC.
  *
- * The plain form uses a library-owned workspace (grown on demand, freed by
- * dash_release_workspace), runs on the default stream and SYNCHRONIZES before
- * returning so that it can report DASH_ERR_TIMEOUT.
+ * The plain form uses a library-owned workspace on the current device (one
+ * per device, grown on demand, freed by dash_release_workspace), runs on the
+ * default stream and SYNCHRONIZES before returning so that it can report
+ * DASH_ERR_TIMEOUT.  Calls from several host threads take turns on it.
  */
 int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dO,
                   const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,
@@ -321,7 +322,8 @@ int dash_schedule_table(int schedule, int heads, int N, int d, int causal, int p
                         int* task_kv, int* task_q, int* rank);
 
 const char* dash_last_error(void);
-/* Frees the library-owned workspace of dash_attn_bwd (next call reallocates). */
+/* Frees the library-owned workspaces of dash_attn_bwd on every device (the
+   next call reallocates on its device). */
 void dash_release_workspace(void);
 
 #ifdef __cplusplus

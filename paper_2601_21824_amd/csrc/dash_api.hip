@@ -376,8 +376,13 @@ int auto_pick(int B, int H, int N, int d, int causal, long resident, int* sched,
   return DASH_OK;
 }
 
-void* g_ws = nullptr;
-size_t g_ws_bytes = 0;
+// The workspace of the non-_ex backward, one per device (grown on demand,
+// freed by dash_release_workspace): a call uses the current device's.
+struct CachedWorkspace {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+CachedWorkspace g_ws[64];
 std::mutex g_ws_mu;
 
 }  // namespace
@@ -596,20 +601,25 @@ int dash_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
   int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
   if (rc) return rc;
   if ((size_t)B * H * N == 0) return DASH_OK;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DASH_ERR_NO_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(DASH_ERR_NO_DEVICE, "device index out of range");
   std::lock_guard<std::mutex> lk(g_ws_mu);
+  CachedWorkspace& ws = g_ws[dev];
   const size_t need = layout(B, H, N, d, resolve(schedule, d, causal)).total;
-  if (g_ws_bytes < need) {
-    if (g_ws) (void)hipFree(g_ws);
-    g_ws = nullptr;
-    g_ws_bytes = 0;
-    hipError_t e = hipMalloc(&g_ws, need);
+  if (ws.bytes < need) {
+    if (ws.p) (void)hipFree(ws.p);
+    ws.p = nullptr;
+    ws.bytes = 0;
+    e = hipMalloc(&ws.p, need);
     if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
-    g_ws_bytes = need;
+    ws.bytes = need;
   }
-  rc = dash_attn_bwd_ex(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale, g_ws,
-                        g_ws_bytes, nullptr, nullptr);
+  rc = dash_attn_bwd_ex(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale, ws.p, ws.bytes,
+                        nullptr, nullptr);
   if (rc) return rc;
-  return dash_bwd_check(g_ws, nullptr);
+  return dash_bwd_check(ws.p, nullptr);
 }
 
 int dash_auto_schedule(int B, int H, int N, int d, int causal, int workers, int* schedule, double* predicted_ms) {
@@ -700,9 +710,16 @@ int dash_mfma_peak(int iters, double* tflops) {
 
 void dash_release_workspace(void) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
-  if (g_ws) (void)hipFree(g_ws);
-  g_ws = nullptr;
-  g_ws_bytes = 0;
+  int cur = -1;
+  const bool restore = hipGetDevice(&cur) == hipSuccess;
+  for (int dev = 0; dev < 64; ++dev) {
+    CachedWorkspace& ws = g_ws[dev];
+    if (!ws.p) continue;
+    if (hipSetDevice(dev) == hipSuccess) (void)hipFree(ws.p);
+    ws.p = nullptr;
+    ws.bytes = 0;
+  }
+  if (restore) (void)hipSetDevice(cur);
 }
 
 int dash_schedule_table(int schedule, int heads, int N, int d, int causal, int placement, int* geometry,

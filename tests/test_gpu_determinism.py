@@ -452,3 +452,22 @@ def test_bad_arguments_on_device():
     with pytest.raises(dash.DashError) as e:
         dash.attn_bwd(qg, kg, vg, og, dog, lseg, False, "shift", workspace=ws)
     assert e.value.code == dash.DASH_ERR_INVALID_ARG
+
+
+def test_plain_form_workspace_is_cached_and_released():
+    """The plain dash_attn_bwd (no workspace argument) runs on the library's
+    own workspace of the current device: bitwise the result of the same
+    schedule on a caller workspace, at a shape that grows the cached one, and
+    again after dash_release_workspace freed it."""
+    for B, H, N, d, causal, sched in ((1, 2, 512, 64, False, "shift"), (2, 4, 1500, 128, True, "descending"),
+                                      (1, 2, 512, 64, False, "shift")):
+        print(f"\n[plain] B={B} H={H} N={N} d={d} causal={causal} {sched}", flush=True)
+        q, k, v, do, (qg, kg, vg, dog) = inputs(B, H, N, d, 77 + N)
+        og, lseg = run_fwd(qg, kg, vg, causal)
+        want = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched, workspace=dash.new_workspace(B, H, N, d, sched))
+        got = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
+        for a, b in zip(got, want):
+            assert torch.equal(a, b)
+        if N == 1500:
+            dash.dash_release_workspace()
+    dash.dash_release_workspace()
