@@ -471,3 +471,21 @@ def test_plain_form_workspace_is_cached_and_released():
         if N == 1500:
             dash.dash_release_workspace()
     dash.dash_release_workspace()
+
+
+@pytest.mark.parametrize("shape", [(0, 2, 128, 64), (1, 0, 128, 128), (2, 3, 0, 256)],
+                         ids=["B0", "H0", "N0"])
+def test_empty_problems_are_no_ops(shape):
+    """A call with no rows (B, H or N zero) returns DASH_OK in every form
+    without touching memory: zero-size tensors may carry null pointers."""
+    B, H, N, d = shape
+    q = torch.empty((B, H, N, d), dtype=torch.bfloat16, device="cuda")
+    o, lse = dash.attn_fwd(q, q, q, False)
+    assert o.shape == q.shape and lse.shape == (B, H, N)
+    for causal in (False, True):
+        for sched in ("atomic", "naive", "descending", "shift", "auto") + (("partials", "split") if d <= 128 else ()):
+            dash.attn_bwd(q, q, q, o, q, lse, causal, sched)
+            ws = dash.new_workspace(B, H, N, d, sched)
+            dash.attn_bwd(q, q, q, o, q, lse, causal, sched, workspace=ws)
+            assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    torch.cuda.synchronize()
