@@ -224,7 +224,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the backward shards over heads with no communication, "
-              "and this build runs on a single MI355X; use --gpus 1", file=sys.stderr)
+              "so a run on N GPUs is N independent single-GPU runs; use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -74,7 +74,7 @@ typedef enum {
 typedef enum {
   DASH_OK = 0,
   DASH_ERR_INVALID_ARG = -1, /* null pointer, negative size, d not 64/128/256, bad enum */
-  DASH_ERR_UNSUPPORTED = -2, /* valid request this build cannot run (e.g. SYMSHIFT
+  DASH_ERR_UNSUPPORTED = -2, /* valid request the library cannot run (e.g. SYMSHIFT
                                 with a full mask, too many KV tiles per head) */
   DASH_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
   DASH_ERR_TIMEOUT = -4,     /* an ordering wait exceeded its spin limit; outputs
