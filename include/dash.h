@@ -204,6 +204,9 @@ size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule);
  * ws_bytes >= dash_bwd_workspace_size(B,H,N,d,schedule) bytes (256-byte aligned).  The
  * workspace must not be used by another call until this one has finished.
  * A wait timeout is recorded in the workspace; read it with dash_bwd_check.
+ * A call with no rows (B, H or N zero) computes nothing and may pass null
+ * tensors and workspace; given a workspace, it only resets its error flag
+ * (one lane of one workgroup on `stream`).
  * Shift and Symmetric Shift chains wait on each other in a cycle (Section
  * 3.1 assumes one KV tile per SM, all running at once): their main kernel is
  * launched cooperatively, so a grid the device cannot keep resident at once
@@ -231,7 +234,8 @@ int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o,
  * must start at zero themselves (no memset is recorded).  status: optional
  * caller-owned device int; the call sets it to 0, or to 1 if an ordering wait
  * timed out (outputs then undefined) -- read it once the stream has finished
- * the call.  Argument errors as dash_attn_bwd_ex.
+ * the call; a call with no rows only sets it to 0.  Argument errors as
+ * dash_attn_bwd_ex.
  */
 int dash_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dO,
                           const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d, int causal,

@@ -84,6 +84,18 @@ struct DeviceInfo {
   int nxcd = 0;  // XCDs, when workgroup i runs on XCD i % nxcd (0: not usable for XCD-local placement)
 };
 
+// A call with no rows still reports "no timeout": one lane stores 0 into the
+// workspace's error flag and / or the caller's status word (a kernel, not a
+// memset, so that the call stays capturable into a HIP graph).
+__global__ void clear_flags_kernel(int* flag, int* status) {
+  if (threadIdx.x == 0) {
+    if (flag) *flag = 0;
+    if (status) *status = 0;
+  }
+}
+
+int clear_flags(int* flag, int* status, void* stream);
+
 // Each workgroup records the XCD it runs on.
 __global__ void xcc_probe_kernel(int* out) {
   unsigned x;
@@ -425,6 +437,13 @@ int dash_attn_fwd(const void* q, const void* k, const void* v, void* o, float* l
 
 namespace {
 
+int clear_flags(int* flag, int* status, void* stream) {
+  if (!flag && !status) return DASH_OK;
+  hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, flag, status);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? DASH_OK : hip_fail(e, "flag reset launch");
+}
+
 // The backward on `workspace` (dash_attn_bwd_ex's contract); `status`, if
 // non-null, is a device int that bwd_pre zeroes and a wait timeout sets.
 int bwd_launch(const void* q, const void* k, const void* v, const void* o, const void* dO, const float* lse,
@@ -434,7 +453,11 @@ int bwd_launch(const void* q, const void* k, const void* v, const void* o, const
   if (scale == 0.f && d > 0) scale = 1.0f / std::sqrt((float)d);
   int rc = check_bwd(q, k, v, o, dO, lse, dq, dk, dv, B, H, N, d, causal, schedule, scale);
   if (rc) return rc;
-  if ((size_t)B * H * N == 0) return DASH_OK;
+  if ((size_t)B * H * N == 0) {
+    // nothing to compute; the workspace's error flag and `status` still read "no timeout"
+    int* flag = workspace && ws_bytes >= dash::kCtrlBytes ? (int*)workspace + dash::kCtrlError : nullptr;
+    return clear_flags(flag, status, stream);
+  }
   const Layout L = layout(B, H, N, d, resolve(schedule, d, causal));
   if (!workspace || ws_bytes < L.total)
     return fail(DASH_ERR_INVALID_ARG, "workspace missing or smaller than dash_bwd_workspace_size()");
@@ -570,7 +593,10 @@ int dash_attn_bwd_noalloc(const void* q, const void* k, const void* v, const voi
                           int schedule, float scale, int* status, void* stream) {
   int rc = check_shape(B, H, N, d);
   if (rc) return rc;
-  if ((size_t)B * H * N == 0) return DASH_OK;
+  if ((size_t)B * H * N == 0) {
+    if ((rc = check_schedule(schedule, causal))) return rc;
+    return clear_flags(nullptr, status, stream);
+  }
   const size_t need = dash_bwd_workspace_size(B, H, N, d, schedule);
   if (need == 0) return fail(DASH_ERR_INVALID_ARG, "unknown schedule");
   if (need > kScratchBytes)

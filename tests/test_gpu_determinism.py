@@ -477,7 +477,10 @@ def test_plain_form_workspace_is_cached_and_released():
                          ids=["B0", "H0", "N0"])
 def test_empty_problems_are_no_ops(shape):
     """A call with no rows (B, H or N zero) returns DASH_OK in every form
-    without touching memory: zero-size tensors may carry null pointers."""
+    (zero-size tensors may carry null pointers) and computes nothing; given a
+    workspace, it resets the workspace's error flag, so dash_bwd_check reads
+    OK even on a workspace no call has used; the allocation-free form sets its
+    status word to 0."""
     B, H, N, d = shape
     q = torch.empty((B, H, N, d), dtype=torch.bfloat16, device="cuda")
     o, lse = dash.attn_fwd(q, q, q, False)
@@ -486,6 +489,12 @@ def test_empty_problems_are_no_ops(shape):
         for sched in ("atomic", "naive", "descending", "shift", "auto") + (("partials", "split") if d <= 128 else ()):
             dash.attn_bwd(q, q, q, o, q, lse, causal, sched)
             ws = dash.new_workspace(B, H, N, d, sched)
+            ws.fill_(0xA5)  # what a fresh allocation may hold: the flag reads "timed out"
             dash.attn_bwd(q, q, q, o, q, lse, causal, sched, workspace=ws)
             assert dash.dash_bwd_check(ws) == dash.DASH_OK
+            status = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+            dash.dash_attn_bwd_noalloc(q, q, q, o, q, lse, *(torch.empty_like(q) for _ in range(3)), causal,
+                                       sched, status=status)
+            torch.cuda.synchronize()
+            assert int(status.item()) == 0
     torch.cuda.synchronize()
