@@ -127,13 +127,13 @@ def measured_traffic():
     the counters were taken."""
     import hashlib
     summary = os.path.join(ROOT, "profiles", "bwd_main_b2h16n8192d128_full.md")
-    src = os.path.join(ROOT, "paper_2601_21824_amd", "csrc", "attn_bwd.hip")
     try:
         text = open(summary).read()
+        fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
+        src = os.path.join(ROOT, fields["source_file"].strip())
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    except OSError:
+    except (OSError, KeyError):
         return None
-    fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
     if fields.get("source_sha256_prefix", "").strip() != sha:
         return None
     return float(fields["traffic_bytes_per_launch"])

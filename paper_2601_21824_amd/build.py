@@ -12,9 +12,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libdash.so")
-SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd64w.hip", "attn_bwd256.hip", "attn_dq.hip", "mfma_peak.hip",
+SOURCES = ["attn_fwd.hip", "attn_bwd.hip", "attn_bwd_d64.hip", "attn_bwd64w.hip", "attn_bwd256.hip", "attn_dq.hip", "mfma_peak.hip",
            "dash_api.hip"]
-HEADERS = ["common.h", "kernels.h", "schedule.h", "bwd_common.h", "lds_layout.h", "dag_model.h", "model_calibration.h"]
+HEADERS = ["common.h", "kernels.h", "schedule.h", "bwd_common.h", "bwd_main.h", "lds_layout.h", "dag_model.h", "model_calibration.h"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -23,12 +23,13 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
 ]
-# per-source flags: the 256-row d = 64 kernel runs faster with its MFMA
-# results in VGPRs (S and dP feed the softmax without AGPR reads), and the
-# d = 256 kernel compiles that way without the VGPR spills (and scratch) it
-# has otherwise; the d = 128 kernel, with less room in its VGPRs, runs slower
+# per-source flags: the d = 64 kernels (128- and 256-row tiles) run faster
+# with their MFMA results in VGPRs (S and dP feed the softmax without AGPR
+# reads), and the d = 256 kernel compiles that way without the VGPR spills
+# (and scratch) it has otherwise; the d = 128 kernel, with less room in its
+# VGPRs, runs slower that way
 _VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-SOURCE_FLAGS = {"attn_bwd64w.hip": _VGPR_MFMA, "attn_bwd256.hip": _VGPR_MFMA}
+SOURCE_FLAGS = {"attn_bwd_d64.hip": _VGPR_MFMA, "attn_bwd64w.hip": _VGPR_MFMA, "attn_bwd256.hip": _VGPR_MFMA}
 
 
 def hipcc() -> str:

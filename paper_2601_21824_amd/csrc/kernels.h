@@ -72,6 +72,8 @@ hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream
 hipError_t launch_dq(const BwdArgs& a, int d, hipStream_t stream);  // SPLIT's dQ pass (attn_dq.hip)
 int bwd_main_occupancy(int d);
 // head dim 64 (attn_bwd64w.hip)
+hipError_t launch_main64(const BwdArgs& a, int grid_main, hipStream_t stream);
+int main64_occupancy();
 hipError_t launch_main64w(const BwdArgs& a, int grid_main, hipStream_t stream);
 int bwd_main64w_occupancy();
 // head dim 256 (attn_bwd256.hip)
