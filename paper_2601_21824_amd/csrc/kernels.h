@@ -71,7 +71,7 @@ hipError_t launch_attn_fwd(const FwdArgs& a, int d, hipStream_t stream);
 hipError_t launch_bwd(const BwdArgs& a, int d, int grid_main, hipStream_t stream);
 hipError_t launch_dq(const BwdArgs& a, int d, hipStream_t stream);  // SPLIT's dQ pass (attn_dq.hip)
 int bwd_main_occupancy(int d);
-// head dim 64 (attn_bwd64w.hip)
+// head dim 64: 128-row KV tiles (attn_bwd_d64.hip) and 256-row tiles (attn_bwd64w.hip)
 hipError_t launch_main64(const BwdArgs& a, int grid_main, hipStream_t stream);
 int main64_occupancy();
 hipError_t launch_main64w(const BwdArgs& a, int grid_main, hipStream_t stream);
