@@ -306,7 +306,7 @@ int dash_mfma_peak(int iters, double* tflops);
  * head of length N at head dim d, in a call of `heads` = B*H heads: T_r
  * scheduling Q tiles of br rows and T_c KV tiles of bc rows (bc = 128 at
  * d = 128 and 64 at d = 256; at d = 64, 256 when the call has at least 256 KV
- * tiles of 256 rows over all heads (causal: 1024 and N >= 2048), else 128 --
+ * tiles of 256 rows over all heads (causal: 512 and N >= 1024), else 128 --
  * so the summation order depends on the call's number of heads at d = 64),
  * under `placement` (DASH_PLACEMENT_GLOBAL or DASH_PLACEMENT_XCD; only
  * Shift's groups depend on it).  Writes, when the pointer is non-NULL:

@@ -67,14 +67,14 @@ struct Geom {
 // rows per KV tile: 128 at d = 128, 64 at d = 256.  At d = 64, 256 (the
 // 256-row kernel, half the accumulator traffic per FLOP) when the call has
 // KV tiles enough to keep a 256-CU GPU busy -- at least 256 of them over all
-// `heads` heads for a full mask, 1024 and N >= 2048 for a causal one (whose
+// `heads` heads for a full mask, 512 and N >= 1024 for a causal one (whose
 // chains are uneven) -- else 128.  The tile size is part of the summation
 // order, so it is a function of the problem (d, mask, N, heads) alone, never
 // of the device.
 DASH_HD int kv_tile_rows(int d, int causal, int N, long heads) {
   if (d == 64) {
     const long wide = heads * (long)((N + 255) / 256);
-    return (causal ? (N >= 2048 && wide >= 1024) : wide >= 256) ? 256 : 128;
+    return (causal ? (N >= 1024 && wide >= 512) : wide >= 256) ? 256 : 128;
   }
   return d == 128 ? 128 : 64;
 }

@@ -116,11 +116,11 @@ def test_schedule_table_matches_oracle(heads, sched, causal, N, d, placement):
     t_r, t_c, br, bc, grp = tab["t_r"], tab["t_c"], tab["br"], tab["bc"], tab["group"]
     # tile sizes: KV tiles of 128 rows at d = 128, 64 at d = 256, and at d = 64
     # 256 rows when the call has enough of them (full: 256 over all heads;
-    # causal: 1024 and N >= 2048), else 128; Q tiles of 64 rows (full) or
+    # causal: 512 and N >= 1024), else 128; Q tiles of 64 rows (full) or
     # KV-tile rows (causal); Shift groups of at most 256 chains, 32 when every
     # chain of a head runs on one XCD
     wide = heads * -(-N // 256)
-    bc64 = 256 if ((N >= 2048 and wide >= 1024) if causal else wide >= 256) else 128
+    bc64 = 256 if ((N >= 1024 and wide >= 512) if causal else wide >= 256) else 128
     assert bc == {64: bc64, 128: 128, 256: 64}[d]
     assert br == (bc if causal else 64) and t_r * br == t_c * bc
     most = 32 if placement == b.DASH_PLACEMENT_XCD else 256
