@@ -211,8 +211,12 @@ size_t dash_bwd_workspace_size(int B, int H, int N, int d, int schedule);
  * 3.1 assumes one KV tile per SM, all running at once): their main kernel is
  * launched cooperatively, so a grid the device cannot keep resident at once
  * (e.g. while other work occupies its CUs) is refused at launch with
- * DASH_ERR_UNSUPPORTED instead of spinning into the wait watchdog.  The other
- * schedules wait only on chains that started earlier.
+ * DASH_ERR_UNSUPPORTED instead of spinning into the wait watchdog.  While one
+ * process that has made cooperative launches is alive, the runtime refuses
+ * another process's cooperative launch on the same GPU ("the operation cannot
+ * be performed in the present state"): its Shift / Symmetric Shift calls fail
+ * with DASH_ERR_HIP.  The other schedules wait only on chains that started
+ * earlier and launch normally.
  */
 int dash_attn_bwd_ex(const void* q, const void* k, const void* v, const void* o, const void* dO,
                      const float* lse, void* dq, void* dk, void* dv, int B, int H, int N, int d,

@@ -498,3 +498,70 @@ def test_empty_problems_are_no_ops(shape):
             torch.cuda.synchronize()
             assert int(status.item()) == 0
     torch.cuda.synchronize()
+
+
+_CHILD = r"""
+import hashlib, sys
+sys.path.insert(0, {root!r}); sys.path.insert(0, {tests!r})
+import torch
+from gpu_util import inputs, run_fwd, run_bwd
+from paper_2601_21824_amd import binding as dash
+_, _, _, _, (qg, kg, vg, dog) = inputs(2, 4, 1500, 128, 2024)
+og, lseg = run_fwd(qg, kg, vg, {causal})
+out = run_bwd(qg, kg, vg, og, dog, lseg, {causal}, {sched!r})
+h = hashlib.sha256()
+for t in (og, lseg) + tuple(out):
+    h.update(t.cpu().contiguous().view(torch.uint8).numpy().tobytes())
+print(h.hexdigest())
+"""
+
+
+@pytest.mark.parametrize("causal,sched", [(False, "naive"), (True, "descending")])
+def test_bits_identical_across_processes(causal, sched):
+    """The forward and backward outputs of a call hash the same in a fresh
+    process as in this one: nothing in the result depends on the process
+    (work tickets, allocation addresses, timing).  Schedules without a
+    cooperative launch: while this process is alive, a second process's
+    cooperative launch is refused on this platform (Shift and Symmetric
+    Shift then fail with DASH_ERR_HIP; see dash_attn_bwd_ex)."""
+    import hashlib
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    _, _, _, _, (qg, kg, vg, dog) = inputs(2, 4, 1500, 128, 2024)
+    og, lseg = run_fwd(qg, kg, vg, causal)
+    out = run_bwd(qg, kg, vg, og, dog, lseg, causal, sched)
+    h = hashlib.sha256()
+    for t in (og, lseg) + tuple(out):
+        h.update(t.cpu().contiguous().view(torch.uint8).numpy().tobytes())
+    code = _CHILD.format(root=root, tests=os.path.join(root, "tests"), causal=causal, sched=sched)
+    p = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=240)
+    assert p.returncode == 0, p.stderr[-2000:]
+    assert p.stdout.strip().splitlines()[-1] == h.hexdigest()
+
+
+@pytest.mark.parametrize("sched", ["naive", "descending"])
+def test_concurrent_calls_on_two_streams(sched):
+    """Two backward calls running at the same time on two streams, each with
+    its own workspace, give the bits of the same calls run one after the
+    other (the two persistent grids share the CUs; naive and Descending wait
+    only on earlier tickets of their own launch)."""
+    B, H, N, d = 2, 8, 2048, 128
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, 55)
+    _, _, _, _, (qg2, kg2, vg2, dog2) = inputs(B, H, N, d, 56)
+    og, lseg = run_fwd(qg, kg, vg, True)
+    og2, lseg2 = run_fwd(qg2, kg2, vg2, True)
+    want = run_bwd(qg, kg, vg, og, dog, lseg, True, sched, workspace=dash.new_workspace(B, H, N, d, sched))
+    want2 = run_bwd(qg2, kg2, vg2, og2, dog2, lseg2, True, sched, workspace=dash.new_workspace(B, H, N, d, sched))
+    ws, ws2 = dash.new_workspace(B, H, N, d, sched), dash.new_workspace(B, H, N, d, sched)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        got = dash.attn_bwd(qg, kg, vg, og, dog, lseg, True, sched, workspace=ws)
+    with torch.cuda.stream(s2):
+        got2 = dash.attn_bwd(qg2, kg2, vg2, og2, dog2, lseg2, True, sched, workspace=ws2)
+    torch.cuda.synchronize()
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK and dash.dash_bwd_check(ws2) == dash.DASH_OK
+    for a, b in zip(got + got2, want + want2):
+        assert torch.equal(a, b)
