@@ -41,6 +41,7 @@ DET_CASES = [  # (B, H, N, d, causal, schedule[, placement])
     (1, 128, 400, 64, False, "shift"),
     (1, 128, 2100, 64, True, "descending"),
     (1, 128, 2100, 64, True, "symshift"),
+    (2, 64, 1030, 64, True, "descending"),
     (2, 32, 8192, 64, False, "shift"),
 ]
 
@@ -276,6 +277,9 @@ PLACE_CASES = [
     (2, 32, 2048, 64, False, "shift"),
     (2, 32, 2048, 64, False, "naive"),
     (1, 128, 2048, 64, True, "descending"),
+    # causal d = 64 at N = 1024 with 256-row tiles (128 heads x 4 tiles)
+    (1, 128, 1024, 64, True, "symshift"),
+    (1, 128, 1024, 64, True, "naive"),
 ]
 
 
