@@ -39,6 +39,8 @@ CASES = [
     # (attn_bwd64w.hip), ragged last tile
     (1, 128, 400, 64, False),
     (1, 256, 33, 64, False),
+    # causal d = 64 with 256-row tiles from N = 1024 (128 heads x 5 tiles, ragged)
+    (1, 128, 1030, 64, True),
 ]
 
 _cache = {}
