@@ -52,13 +52,24 @@ inline HeadDag build_head_dag(const Geom& G, int N) {
     }
     h.off[w + 1] = (int)blk.size();
   }
-  // each block's contributions sorted by rank: the previous one is the predecessor
-  std::vector<int> idx(blk.size());
-  for (size_t s = 0; s < idx.size(); ++s) idx[s] = (int)s;
-  std::sort(idx.begin(), idx.end(), [&](int a, int b) { return blk[a] != blk[b] ? blk[a] < blk[b] : rnk[a] < rnk[b]; });
+  // each block's contributions in rank order: the previous one is the
+  // predecessor (a table over (block, rank): ranks are below T_c and every
+  // (block, rank) pair occurs at most once)
+  int nb = 0;
+  for (int pb : blk) nb = pb + 1 > nb ? pb + 1 : nb;
+  const size_t tc = (size_t)G.t_c;
+  std::vector<int> at((size_t)nb * tc, -1);
+  for (size_t s = 0; s < blk.size(); ++s) at[(size_t)blk[s] * tc + rnk[s]] = (int)s;
   h.pred.assign(blk.size(), -1);
-  for (size_t k = 1; k < idx.size(); ++k)
-    if (blk[idx[k]] == blk[idx[k - 1]]) h.pred[idx[k]] = idx[k - 1];
+  for (int pb = 0; pb < nb; ++pb) {
+    int prev = -1;
+    for (size_t r = 0; r < tc; ++r) {
+      const int s = at[(size_t)pb * tc + r];
+      if (s < 0) continue;
+      h.pred[s] = prev;
+      prev = s;
+    }
+  }
   return h;
 }
 
