@@ -215,6 +215,9 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
 
       const int nst = next_valid(st + 1);
       const int pb_next = nst < nsteps ? (int)(step_at(nst) & 0xfff) : -1;
+      // the chain moves to another KV tile after this step (Symmetric Shift,
+      // between its two tiles)
+      const bool tile_ends = nst < nsteps && (int)((step_at(nst) >> 12) & 0x1ff) != j;
       int* ctr = ctr_head + (size_t)pb * kCtrStride;
       bool have_turn = false;
 
@@ -403,7 +406,11 @@ __global__ __launch_bounds__(NT) void bwd_main256_kernel(BwdArgs a) {
         }
         if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
         pend_ctr = pb;
-        if (!deferred || nst >= nsteps) {
+        // at the end of the chain or of its KV tile the release comes now: the
+        // tile switch (dK, dV stores, K, V loads) would hold it back, and under
+        // Symmetric Shift every later contributor of the block, one task behind
+        // the one before, would wait for its own predecessor's switch in turn
+        if (!deferred || nst >= nsteps || tile_ends) {
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           release();
         }

@@ -268,6 +268,9 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
       // ---- the next valid block (prefetched into the other buffer below)
       const int nst = next_valid(st + 1);
       const int pb_next = nst < nsteps ? (int)(step_at(nst) & 0xfff) : -1;
+      // the chain moves to another KV tile after this step (Symmetric Shift,
+      // between its two tiles)
+      const bool tile_ends = nst < nsteps && (int)((step_at(nst) >> 12) & 0x1ff) != j;
 
       int* ctr = ctr_head + (size_t)pb * kCtrStride;
       bool have_turn = false;
@@ -594,7 +597,11 @@ __global__ __launch_bounds__(256) void bwd_main_kernel(BwdArgs a) {
           if (tid == 0 && a.witness && rank < a.tc) a.witness[((size_t)bh * a.nblk + pb) * a.tc + rank] = j;
           if (w == 0 && a.witness && rank < a.tc) vm_poll += 1;
           pend_ctr = pb;
-          if (!deferred || nst >= nsteps) {
+          // at the end of the chain or of its KV tile the release comes now: the
+          // tile switch (dK, dV stores, K, V loads) would hold it back, and under
+          // Symmetric Shift every later contributor of the block, one task behind
+          // the one before, would wait for its own predecessor's switch in turn
+          if (!deferred || nst >= nsteps || tile_ends) {
             vm_wait<0>();  // the copy of the next counter has landed as well
             release();
             vm_poll = 63;
