@@ -13,7 +13,7 @@ the two is kept.  One JSON line per shape on stdout, in the format of
     python -m paper_2601_21824_amd.measure_model_grid > paper_2601_21824_amd/model_grid.jsonl
 
 (Head dims as arguments measure only those, e.g. ``... measure_model_grid 64``;
-``--heads 32,128`` only those head counts.)
+``--heads 32,128`` only those head counts, ``--mask causal`` only that mask.)
 """
 from __future__ import annotations
 
@@ -27,10 +27,10 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADS = (1, 4, 16, 32, 64, 128, 256, 512, 1024)
 
 
-def shapes(dims=(64, 128, 256), heads=HEADS):
+def shapes(dims=(64, 128, 256), heads=HEADS, masks=(False, True)):
     for d in dims:
         lengths = (4096, 8192, 16384, 32768) if d == 256 else (512, 1024, 2048, 4096, 8192, 16384)
-        for causal in (False, True):
+        for causal in masks:
             for n in lengths:
                 for bh in heads:
                     flops = 4.0 * bh * n * n * d * 2.5 / (2 if causal else 1)
@@ -51,8 +51,13 @@ def main(*dims):
         i = dims.index("--heads")
         heads = tuple(int(x) for x in dims[i + 1].split(","))
         dims = dims[:i] + dims[i + 2:]
+    masks = (False, True)
+    if "--mask" in dims:
+        i = dims.index("--mask")
+        masks = (dims[i + 1] == "causal",)
+        dims = dims[:i] + dims[i + 2:]
     ev = bench.HipEvents()
-    for d, causal, N, bh in shapes(tuple(int(x) for x in dims) or (64, 128, 256), heads):
+    for d, causal, N, bh in shapes(tuple(int(x) for x in dims) or (64, 128, 256), heads, masks):
         q, k, v, do = make_inputs(1, bh, N, d, seed=N + d + bh, sigma=0.5 if d == 256 else 1.0)
         qg, kg, vg, dog = (t.cuda() for t in (q, k, v, do))
         og, lseg = dash.attn_fwd(qg, kg, vg, causal)
