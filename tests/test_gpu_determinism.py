@@ -37,6 +37,10 @@ DET_CASES = [  # (B, H, N, d, causal, schedule[, placement])
     (2, 16, 8192, 128, False, "shift"),
     (2, 32, 8192, 128, True, "descending"),
     (2, 32, 8192, 128, True, "symshift"),
+    # the long-sequence workload (8 heads of 32768 rows at d = 256): Symmetric
+    # Shift's 256 chains per head change KV tiles half way, releasing the
+    # block before the switch at the end of the tile
+    (1, 8, 32768, 256, True, "symshift"),
     # d = 64 with 256-row KV tiles
     (1, 128, 400, 64, False, "shift"),
     (1, 128, 2100, 64, True, "descending"),
