@@ -101,6 +101,32 @@ def test_serialized_schedules_never_miss_a_turn(case):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"call {r + 2} differs"
 
 
+def test_symmetric_shift_releases_before_its_tile_switch():
+    """A Symmetric Shift chain changes KV tiles once, after the upper-left
+    triangle.  The block it finishes just before the switch is released at
+    once, not after the switch's dK/dV stores and K/V loads: held back, that
+    release made every later contributor of a Q tile in the triangle wait for
+    its predecessor's switch in turn, and the waits grew along the line
+    (9.6% of the wave time at B=2 H=32 N=8192 d=128; 0.6% since).  Checked
+    through the instrumented kernel's ordering-wait share, with a margin."""
+    B, H, N, d = 2, 32, 8192, 128
+    print(f"\n[symshift waits] B={B} H={H} N={N} d={d}", flush=True)
+    _, _, _, _, (qg, kg, vg, dog) = inputs(B, H, N, d, seed=9)
+    og, lseg = run_fwd(qg, kg, vg, True)
+    ws = dash.new_workspace(B, H, N, d, "symshift")
+    for _ in range(5):  # device clock up
+        run_bwd(qg, kg, vg, og, dog, lseg, True, "symshift", workspace=ws)
+    stats = torch.zeros(3, dtype=torch.int64, device="cuda")
+    opts = dash.dash_bwd_options_t(0, 0, None, None, None, None, None, 0, 0, 0, stats.data_ptr())
+    run_bwd(qg, kg, vg, og, dog, lseg, True, "symshift", workspace=ws, options=opts)
+    assert dash.dash_bwd_check(ws) == dash.DASH_OK
+    late, wait_ticks, wave_ticks = (int(x) for x in stats.cpu())
+    assert wave_ticks > 0
+    share = wait_ticks / wave_ticks
+    print(f"[symshift waits] wait share {share:.4f}, late wave-steps {late}", flush=True)
+    assert share < 0.04, f"Symmetric Shift waits {share:.1%} of its wave time"
+
+
 @pytest.mark.parametrize("N,d", [(1024, 64), (2048, 128)])
 def test_naive_and_descending_give_identical_dq(N, d):
     """Both sum every dQ tile in ascending KV order from identical partials."""
