@@ -2,7 +2,7 @@
 behind the block-step times of the DAG model that picks DASH_SCHED_AUTO.
 
 For d in (64, 128, 256), both masks, N from 512 to 16384 (d = 256: 4096 to
-32768) and B*H of 1, 4, 16, 32, 64, 128, 256, 512 and 1024 heads (at most
+32768) and B*H of 1, 2, 4, 16, 32, 64, 128, 256, 512 and 1024 heads (at most
 2^21 tokens and 6e13 FLOPs per call), every
 candidate deterministic schedule is timed as bench.py times a backward call
 (whole call, wall clock over back-to-back calls after 3 checked warm-up
@@ -24,7 +24,7 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-HEADS = (1, 4, 16, 32, 64, 128, 256, 512, 1024)
+HEADS = (1, 2, 4, 16, 32, 64, 128, 256, 512, 1024)
 
 
 def shapes(dims=(64, 128, 256), heads=HEADS, masks=(False, True)):
